@@ -1,0 +1,129 @@
+"""Network-level oracle: a ResNet backbone executed block-sparsely frame by frame.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+In single-stage networks every convolution layer is made block-sparse (Section 4,
+first paragraph), all layers of a frame share the frame's execution grid A_t
+(Section 3.5), each layer keeps its own stored representation (Section 3.1), and
+the first frame of a clip is executed completely (Section 4, BlockCopy
+configuration). Layers run in network order: layer l reads layer l-1's buffer after
+it has been updated for this frame.
+
+The backbones are the standard ResNet-18 / ResNet-50 feature extractors (He et al.,
+2016) with the stride of a downsampling bottleneck on its 3x3 convolution (the
+torchvision convention), batch normalisation folded into the convolutions, and
+no classifier. The layer table below is written here from that definition; the
+HIP runner has its own.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import fold_bn, sparse_conv2d, sparse_maxpool2d, store
+
+
+def resnet_table(depth: int):
+    """List of layers. Each is a dict: kind ('conv'|'pool'), name, src (index of the
+    input layer, -1 = the frame), res (index of the residual layer or None),
+    cin, cout, k, stride, pad, relu."""
+    L = []
+
+    def conv(name, src, cin, cout, k, s, relu, res=None):
+        L.append(dict(kind="conv", name=name, src=src, res=res, cin=cin, cout=cout,
+                      k=k, stride=s, pad=k // 2, relu=relu))
+        return len(L) - 1
+
+    x = conv("stem", -1, 3, 64, 7, 2, True)
+    L.append(dict(kind="pool", name="maxpool", src=x, res=None, cin=64, cout=64,
+                  k=3, stride=2, pad=1, relu=False))
+    x = len(L) - 1
+    cin = 64
+    if depth == 50:
+        stages, width, expansion = [3, 4, 6, 3], [64, 128, 256, 512], 4
+    elif depth == 18:
+        stages, width, expansion = [2, 2, 2, 2], [64, 128, 256, 512], 1
+    else:
+        raise ValueError(depth)
+    for si, (nb, wd) in enumerate(zip(stages, width)):
+        for bi in range(nb):
+            s = 2 if (si > 0 and bi == 0) else 1
+            cout = wd * expansion
+            pre = f"layer{si + 1}.{bi}"
+            if bi == 0 and (s != 1 or cin != cout):
+                ds = conv(pre + ".downsample", x, cin, cout, 1, s, False)
+            else:
+                ds = x
+            if depth == 50:
+                a = conv(pre + ".conv1", x, cin, wd, 1, 1, True)
+                b = conv(pre + ".conv2", a, wd, wd, 3, s, True)
+                x = conv(pre + ".conv3", b, wd, cout, 1, 1, True, res=ds)
+            else:
+                a = conv(pre + ".conv1", x, cin, wd, 3, s, True)
+                x = conv(pre + ".conv2", a, wd, cout, 3, 1, True, res=ds)
+            cin = cout
+    return L
+
+
+def make_params(table, seed0=1000, bn_random=False):
+    """Per-conv fp32 OIHW weights (He-normal, seed seed0 + layer index) and BN
+    parameters. Random init uses gamma=1, beta=0, mean=0, var=1 unless bn_random."""
+    import synth
+    params = []
+    for li, l in enumerate(table):
+        if l["kind"] != "conv":
+            params.append(None)
+            continue
+        r = synth.rng(seed0 + li)
+        w = synth.he_normal(r, l["cout"], l["cin"], l["k"], l["k"])
+        c = l["cout"]
+        if bn_random:
+            bn = dict(gamma=r.uniform(0.5, 1.5, c), beta=r.normal(0, 0.1, c),
+                      mean=r.normal(0, 0.1, c), var=r.uniform(0.5, 1.5, c))
+        else:
+            bn = dict(gamma=np.ones(c), beta=np.zeros(c), mean=np.zeros(c), var=np.ones(c))
+        params.append(dict(w=w, **bn))
+    return params
+
+
+def fold_params(table, params, dtype):
+    """BN folded in fp64; weights rounded to the storage dtype (bit patterns),
+    bias rounded to fp32."""
+    out = []
+    for l, p in zip(table, params):
+        if p is None:
+            out.append(None)
+            continue
+        w2, b2 = fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
+        out.append(dict(w_bits=store(w2, dtype), bias=b2.astype(np.float32)))
+    return out
+
+
+def shapes(table, h, w):
+    """Output (C, H, W) of every layer for an input frame of h x w."""
+    out = []
+    for l in table:
+        ih, iw = (h, w) if l["src"] < 0 else out[l["src"]][1:]
+        oh = (ih + 2 * l["pad"] - l["k"]) // l["stride"] + 1
+        ow = (iw + 2 * l["pad"] - l["k"]) // l["stride"] + 1
+        out.append((l["cout"], oh, ow))
+    return out
+
+
+def frame(table, folded, x_bits, mask, prev, dtype):
+    """One frame through the block-sparse network.
+
+    x_bits: the frame, NCHW bit patterns. mask: uint8 [N, Gh, Gw] execution grid.
+    prev: list of previous per-layer buffers (NCHW bit patterns). Returns the new list.
+    """
+    bufs = []
+    for li, l in enumerate(table):
+        src = x_bits if l["src"] < 0 else bufs[l["src"]]
+        if l["kind"] == "pool":
+            y = sparse_maxpool2d(src, mask, prev[li], dtype, l["k"], l["stride"], l["pad"])
+        else:
+            res = None if l["res"] is None else bufs[l["res"]]
+            y = sparse_conv2d(src, folded[li]["w_bits"], mask, prev[li], dtype,
+                              stride=l["stride"], pad=l["pad"], bias=folded[li]["bias"],
+                              residual_bits=res, relu=l["relu"])
+        bufs.append(y)
+    return bufs
