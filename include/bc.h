@@ -1,0 +1,220 @@
+/*
+ * bc.h -- C ABI of the MI355X (gfx950) block-sparse convolution library with
+ * temporal feature copying (BlockCopy, Verelst & Tuytelaars, ICCV 2021).
+ *
+ * What the library computes (Section 3.1 and the caption of Fig. 3): a CNN layer
+ * is executed only on the image blocks that the frame's execution grid selects
+ * (a_b = 1, Section 3.5); every other block keeps the layer's representation from
+ * the previous execution ("feature transfer", a_b = 0). A selected block is
+ * computed with its halo read from its neighbours in the layer's current input,
+ * so that there are no discontinuities between blocks (the BlockPadding idea the
+ * paper builds on, Section 3.1). For one layer this equals
+ *
+ *     out = select(mask, layer(in), out_previous)
+ *
+ * where layer() is the ordinary dense layer and select() keeps out_previous bit
+ * for bit outside the selected blocks. Non-selected blocks of `out` are never
+ * read or written.
+ *
+ * Conventions for every entry point:
+ *  - Pointers named d_* are DEVICE memory owned by the caller. The library never
+ *    allocates, frees or retains caller memory, and never throws or aborts
+ *    across the ABI.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work is
+ *    enqueued asynchronously; no call synchronises except bc_build_block_index
+ *    with a non-NULL h_count.
+ *  - All tensors are dense and contiguous in the stated layout.
+ *  - Every argument check runs before anything is enqueued; on a non-OK status
+ *    nothing was enqueued and no memory was touched. bc_last_error() then holds
+ *    a thread-local description. A fault of earlier asynchronous work surfaces
+ *    as BC_ERR_HIP on a later call.
+ *  - Blocks: the execution grid has grid_h x grid_w blocks per image, the same
+ *    grid for every layer of a network (Section 3.5: one decision per block). A
+ *    layer whose output is H x W has output blocks of edge bh = H / grid_h,
+ *    bw = W / grid_w; H and W must be divisible (else BC_ERR_NOT_DIVISIBLE).
+ *    The grid indexes OUTPUT blocks; the input tile of output block (gy, gx) of
+ *    a layer with kernel kh x kw, stride s and padding p spans input rows
+ *    gy*bh*s - p .. gy*bh*s - p + (bh-1)*s + kh - 1 (same for columns).
+ *  - Active-block index: int32 ids id = (img * grid_h + gy) * grid_w + gx of the
+ *    selected blocks, strictly ascending, with their number in *d_count (device).
+ *    Kernels read the count on the device, so no host round trip is needed.
+ *    Passing d_idx = d_count = NULL to a layer call means "every block" (a full
+ *    frame, as for the first frame of a clip, Section 4).
+ */
+#ifndef BC_H
+#define BC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BC_ABI_VERSION 1
+
+typedef enum {
+    BC_OK = 0,
+    BC_ERR_NULL = 1,          /* a required pointer is NULL                      */
+    BC_ERR_SHAPE = 2,         /* tensor sizes inconsistent with each other/geometry */
+    BC_ERR_DTYPE = 3,         /* dtype mismatch between tensors or unknown dtype  */
+    BC_ERR_LAYOUT = 4,        /* layout mismatch or unknown layout               */
+    BC_ERR_NOT_DIVISIBLE = 5, /* output size not divisible by the block grid     */
+    BC_ERR_CAPACITY = 6,      /* index / packed capacity < n * grid_h * grid_w   */
+    BC_ERR_ALIAS = 7,         /* output overlaps an input                        */
+    BC_ERR_UNINITIALIZED = 8, /* sparse write into a registered, invalid buffer  */
+    BC_ERR_UNSUPPORTED = 9,   /* valid request outside what the kernels implement */
+    BC_ERR_HIP = 10           /* HIP runtime error (launch or earlier async fault) */
+} bc_status;
+
+typedef enum { BC_F32 = 0, BC_BF16 = 1, BC_F16 = 2 } bc_dtype;
+typedef enum { BC_NCHW = 0, BC_NHWC = 1 } bc_layout;
+
+/* Shape and format of a 4-D feature map. dtype is a bc_dtype, layout a bc_layout. */
+typedef struct { int32_t n, c, h, w; int32_t dtype; int32_t layout; } bc_tensor;
+
+/* Block grid per image. */
+typedef struct { int32_t grid_h, grid_w; } bc_grid;
+
+/* Convolution / pooling geometry: kernel kh x kw, stride, zero padding (pooling:
+ * -inf padding), fused ReLU flag (conv only). Dilation and groups are 1. */
+typedef struct { int32_t kh, kw, stride, pad, relu; } bc_conv;
+
+/* ABI version (BC_ABI_VERSION) of the loaded library. */
+int32_t bc_abi_version(void);
+
+/* Static text for a status code. */
+const char *bc_status_str(int32_t status);
+
+/* Thread-local detail of the last non-OK status returned on this thread ("" if none). */
+const char *bc_last_error(void);
+
+/*
+ * Mask -> active-block index (Section 3.5: the execution grid A_t, a_b = 1
+ * executes block b).
+ *   d_mask   uint8 [n][grid_h][grid_w], device; nonzero byte = execute.
+ *   d_idx    int32 [capacity], device, written with the ascending ids of the
+ *            nonzero entries; entries at and beyond the count are left untouched.
+ *   d_count  int32 [1], device, written with the number of nonzero entries.
+ *   h_count  optional host int32; if non-NULL the count is also copied to it and
+ *            the call waits for the stream (the only synchronising call).
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE (n, grid <= 0 or n*grid_h*grid_w > 2^20),
+ * BC_ERR_CAPACITY (capacity < n*grid_h*grid_w), BC_ERR_HIP.
+ */
+bc_status bc_build_block_index(const uint8_t *d_mask, int32_t n, bc_grid g,
+                               int32_t *d_idx, int32_t capacity, int32_t *d_count,
+                               int32_t *h_count, void *stream);
+
+/*
+ * Standalone halo gather (the BlockPadding step, Section 3.1): for the k-th active
+ * output block of a layer with geometry *geom whose input is `src`, copy its input
+ * tile to d_packed[k] = [th][tw][C] (channels last, src dtype), th = (bh-1)*s + kh,
+ * tw = (bw-1)*s + kw, where bh x bw is the output block edge implied by src, geom
+ * and the grid. Positions outside the image get pad_value (rounded to the dtype).
+ *   d_src     src.layout (NCHW or NHWC), any dtype.
+ *   d_packed  [capacity][th][tw][C]; only the first *d_count tiles are written.
+ * d_idx/d_count may both be NULL (every block). Errors: BC_ERR_NULL, BC_ERR_SHAPE,
+ * BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE, BC_ERR_CAPACITY, BC_ERR_ALIAS,
+ * BC_ERR_UNSUPPORTED (stride outside {1,2}, kernel edge outside 1..7), BC_ERR_HIP.
+ */
+bc_status bc_gather_halo(const void *d_src, bc_tensor src, bc_grid g, const bc_conv *geom,
+                         float pad_value, const int32_t *d_idx, const int32_t *d_count,
+                         int32_t capacity, void *d_packed, void *stream);
+
+/*
+ * Standalone scatter into a persistent buffer (Section 3.1, stored representations):
+ * d_packed[k] = [bh][bw][C] (channels last, dst dtype) is written to the position of
+ * the k-th active block of `dst`, bh = dst.h / grid_h, bw = dst.w / grid_w. Every
+ * other element of dst is neither read nor written.
+ * Errors: as bc_gather_halo.
+ */
+bc_status bc_scatter_blocks(const void *d_packed, const int32_t *d_idx, const int32_t *d_count,
+                            int32_t capacity, bc_grid g, void *d_dst, bc_tensor dst,
+                            void *stream);
+
+/*
+ * Block-sparse convolution with fused epilogue (Section 3.1; every conv layer of a
+ * single-stage network, Section 4):
+ *   out[block] = act(conv(in)[block] + bias (+ residual[block]))  for active blocks,
+ *   out[other] untouched (feature transfer).
+ * conv is a cross-correlation with zero padding; act is ReLU when conv->relu.
+ * Arithmetic: products of the stored operands accumulated in fp32, bias and
+ * residual added in fp32, ReLU, then one round-to-nearest-even to out.dtype.
+ *   in, out    same dtype and layout. NHWC: BF16 or F16 (matrix-core path).
+ *              NCHW: F32 (fp32 FMA path).
+ *   d_w        NHWC: [Cout][kh][kw][Cin] in in.dtype. NCHW: [Cout][Cin][kh][kw] F32.
+ *   d_bias     [Cout] fp32 (batch norm folded in, see bc_fold_bn), or NULL.
+ *   d_residual shaped and typed like out, or NULL; read only at active blocks.
+ *   d_out      must not overlap d_in, d_w or d_residual (BC_ERR_ALIAS).
+ * Sizes: out.n = in.n, out.h = (in.h + 2*pad - kh)/stride + 1 (same for w).
+ * Supported: stride 1 or 2; kh = kw in {1, 3, 5, 7}; NHWC needs Cin % 8 == 0 or
+ * kw*Cin <= 32 (the stem form), and Cout % 16 == 0.
+ * If d_out is a registered buffer (bc_buffer_register) that is not valid, a sparse
+ * call (d_idx non-NULL) returns BC_ERR_UNINITIALIZED; a full call (d_idx = d_count
+ * = NULL) makes it valid.
+ */
+bc_status bc_sparse_conv2d(const bc_conv *conv,
+                           const void *d_in, bc_tensor in,
+                           const void *d_w, const float *d_bias, const void *d_residual,
+                           void *d_out, bc_tensor out, bc_grid g,
+                           const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                           void *stream);
+
+/*
+ * Block-sparse max pooling (the ResNet stem pooling run block-sparsely), kernel
+ * kh x kw, stride, padding with -inf (padded positions never win). Same selection
+ * contract, layouts, dtypes and registered-buffer rule as bc_sparse_conv2d; the
+ * relu field is ignored. NaN inputs give unspecified results.
+ */
+bc_status bc_sparse_maxpool2d(const bc_conv *geom, const void *d_in, bc_tensor in,
+                              void *d_out, bc_tensor out, bc_grid g,
+                              const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                              void *stream);
+
+/*
+ * Host only. Fold inference-mode batch normalisation into the preceding conv:
+ * w_out = w * gamma / sqrt(var + eps), b_out = beta + (conv_bias - mean) * gamma /
+ * sqrt(var + eps), computed in double and rounded to float. w is [cout][per_out]
+ * (per_out = everything after the output channel), conv_bias may be NULL (zero).
+ * w_out may equal w (in place). Errors: BC_ERR_NULL, BC_ERR_SHAPE.
+ */
+bc_status bc_fold_bn(const float *w, int32_t cout, int32_t per_out, const float *conv_bias,
+                     const float *gamma, const float *beta, const float *mean,
+                     const float *var, float eps, float *w_out, float *b_out);
+
+/*
+ * Host only. Repack fp32 OIHW weights [cout][cin][kh][kw] into the NHWC weight layout
+ * [cout][kh][kw][cin] of `dtype` (BC_BF16 / BC_F16: round to nearest even;
+ * BC_F32: copy). h_out receives cout*kh*kw*cin elements. Errors: BC_ERR_NULL,
+ * BC_ERR_SHAPE, BC_ERR_DTYPE.
+ */
+bc_status bc_repack_weights(const float *w_oihw, int32_t cout, int32_t cin, int32_t kh,
+                            int32_t kw, int32_t dtype, void *h_out);
+
+/*
+ * Persistent per-layer buffers (Section 3.1: representations throughout the network
+ * are stored and reused). A registration wraps caller memory (it does not copy or
+ * own it) and tracks whether the buffer holds a complete representation: it
+ * starts invalid, becomes valid after a full-frame write, and a sparse write into
+ * an invalid buffer is refused (the first frame of a clip is executed
+ * completely, Section 4).
+ */
+typedef struct bc_buffer_s *bc_buffer;
+
+/* Register d_mem with descriptor desc. Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE,
+ * BC_ERR_LAYOUT, BC_ERR_ALIAS (overlaps a registered buffer). */
+bc_status bc_buffer_register(void *d_mem, bc_tensor desc, bc_buffer *out);
+/* Forget a registration (the memory is the caller's). Errors: BC_ERR_NULL. */
+bc_status bc_buffer_release(bc_buffer b);
+/* Start of a new clip: the next write must be a full one. Errors: BC_ERR_NULL. */
+bc_status bc_buffer_invalidate(bc_buffer b);
+/* Record a write done by other means: full_mask != 0 makes the buffer valid;
+ * full_mask == 0 on an invalid buffer returns BC_ERR_UNINITIALIZED. */
+bc_status bc_buffer_mark_written(bc_buffer b, int32_t full_mask);
+/* 1 if valid, 0 if not, -1 for a NULL or unknown handle. */
+int32_t bc_buffer_is_valid(bc_buffer b);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BC_H */

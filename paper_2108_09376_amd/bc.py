@@ -1,0 +1,258 @@
+"""Python binding of libblockcopy (the C ABI declared in include/bc.h).
+
+Argument marshalling only: every function here has the name of the C entry point it
+calls, takes torch tensors (device memory) or numpy arrays (host memory), and
+passes raw pointers, sizes and the current HIP stream. All computation happens in
+the HIP kernels of the library. There is no fallback: if the library is missing
+or fails to load, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libblockcopy.so")
+
+BC_OK, BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT = 0, 1, 2, 3, 4
+BC_ERR_NOT_DIVISIBLE, BC_ERR_CAPACITY, BC_ERR_ALIAS, BC_ERR_UNINITIALIZED = 5, 6, 7, 8
+BC_ERR_UNSUPPORTED, BC_ERR_HIP = 9, 10
+BC_F32, BC_BF16, BC_F16 = 0, 1, 2
+BC_NCHW, BC_NHWC = 0, 1
+
+
+class BCError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        self.status = status
+        super().__init__(f"{func}: status {status} ({status_name(status)}): {detail}")
+
+
+class bc_tensor(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("c", ctypes.c_int32), ("h", ctypes.c_int32),
+                ("w", ctypes.c_int32), ("dtype", ctypes.c_int32), ("layout", ctypes.c_int32)]
+
+
+class bc_grid(ctypes.Structure):
+    _fields_ = [("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32)]
+
+
+class bc_conv(ctypes.Structure):
+    _fields_ = [("kh", ctypes.c_int32), ("kw", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2108_09376_amd.build` "
+                      "(there is no fallback path)")
+_lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i32, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+_sigs = {
+    "bc_abi_version": ([], _i32),
+    "bc_status_str": ([_i32], ctypes.c_char_p),
+    "bc_last_error": ([], ctypes.c_char_p),
+    "bc_build_block_index": ([_vp, _i32, bc_grid, _vp, _i32, _vp, _vp, _vp], _i32),
+    "bc_gather_halo": ([_vp, bc_tensor, bc_grid, ctypes.POINTER(bc_conv), _f32, _vp, _vp, _i32, _vp,
+                        _vp], _i32),
+    "bc_scatter_blocks": ([_vp, _vp, _vp, _i32, bc_grid, _vp, bc_tensor, _vp], _i32),
+    "bc_sparse_conv2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, _vp, bc_tensor,
+                          bc_grid, _vp, _vp, _i32, _vp], _i32),
+    "bc_sparse_maxpool2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, bc_grid, _vp,
+                             _vp, _i32, _vp], _i32),
+    "bc_fold_bn": ([_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp], _i32),
+    "bc_repack_weights": ([_vp, _i32, _i32, _i32, _i32, _i32, _vp], _i32),
+    "bc_buffer_register": ([_vp, bc_tensor, ctypes.POINTER(_vp)], _i32),
+    "bc_buffer_release": ([_vp], _i32),
+    "bc_buffer_invalidate": ([_vp], _i32),
+    "bc_buffer_mark_written": ([_vp, _i32], _i32),
+    "bc_buffer_is_valid": ([_vp], _i32),
+}
+for _name, (_args, _res) in _sigs.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = _res
+
+EXPORTED = tuple(_sigs)
+
+
+def status_name(s: int) -> str:
+    return _lib.bc_status_str(int(s)).decode()
+
+
+def _check(status: int, func: str):
+    if status != BC_OK:
+        raise BCError(status, func, _lib.bc_last_error().decode())
+
+
+def bc_abi_version() -> int:
+    return int(_lib.bc_abi_version())
+
+
+def bc_last_error() -> str:
+    return _lib.bc_last_error().decode()
+
+
+# ------------------------------------------------------------------ marshalling helpers
+
+_TORCH_DT = {}
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if not _TORCH_DT:
+        _TORCH_DT.update({torch.float32: BC_F32, torch.bfloat16: BC_BF16, torch.float16: BC_F16})
+    return _TORCH_DT[t.dtype]
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def desc(t, layout: int) -> bc_tensor:
+    """bc_tensor of a contiguous 4-D tensor stored NHWC ([N,H,W,C]) or NCHW ([N,C,H,W])."""
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    if t.dim() != 4:
+        raise ValueError("feature maps are 4-D")
+    if layout == BC_NHWC:
+        n, h, w, c = t.shape
+    else:
+        n, c, h, w = t.shape
+    return bc_tensor(n, c, h, w, _dtype_code(t), layout)
+
+
+def _grid(g) -> bc_grid:
+    return g if isinstance(g, bc_grid) else bc_grid(int(g[0]), int(g[1]))
+
+
+def _conv(c) -> bc_conv:
+    return c if isinstance(c, bc_conv) else bc_conv(*[int(v) for v in c])
+
+
+# ------------------------------------------------------------------ entry points
+
+def bc_build_block_index(mask, n, grid, idx, count, h_count=None, stream=None):
+    """mask uint8 [n, gh, gw] (device) -> idx int32 [capacity], count int32 [1] (device).
+    With h_count=True the count is also returned to the host (synchronising)."""
+    hc = ctypes.c_int32(0) if h_count else None
+    st = _lib.bc_build_block_index(_ptr(mask), int(n), _grid(grid), _ptr(idx), int(idx.numel()),
+                                   _ptr(count), ctypes.byref(hc) if hc is not None else None,
+                                   _stream(stream))
+    _check(st, "bc_build_block_index")
+    return hc.value if hc is not None else None
+
+
+def bc_gather_halo(src, layout, grid, geom, pad_value, idx, count, packed, stream=None):
+    cap = 0 if idx is None else int(idx.numel())
+    c = _conv(geom)
+    st = _lib.bc_gather_halo(_ptr(src), desc(src, layout), _grid(grid), ctypes.byref(c),
+                             float(pad_value), _ptr(idx), _ptr(count), cap, _ptr(packed),
+                             _stream(stream))
+    _check(st, "bc_gather_halo")
+
+
+def bc_scatter_blocks(packed, idx, count, grid, dst, layout, stream=None):
+    cap = 0 if idx is None else int(idx.numel())
+    st = _lib.bc_scatter_blocks(_ptr(packed), _ptr(idx), _ptr(count), cap, _grid(grid), _ptr(dst),
+                                desc(dst, layout), _stream(stream))
+    _check(st, "bc_scatter_blocks")
+
+
+def bc_sparse_conv2d(conv, x, layout, w, bias, residual, out, grid, idx, count, stream=None):
+    cap = 0 if idx is None else int(idx.numel())
+    c = _conv(conv)
+    st = _lib.bc_sparse_conv2d(ctypes.byref(c), _ptr(x), desc(x, layout), _ptr(w), _ptr(bias),
+                               _ptr(residual), _ptr(out), desc(out, layout), _grid(grid), _ptr(idx),
+                               _ptr(count), cap, _stream(stream))
+    _check(st, "bc_sparse_conv2d")
+
+
+def bc_sparse_maxpool2d(geom, x, layout, out, grid, idx, count, stream=None):
+    cap = 0 if idx is None else int(idx.numel())
+    c = _conv(geom)
+    st = _lib.bc_sparse_maxpool2d(ctypes.byref(c), _ptr(x), desc(x, layout), _ptr(out),
+                                  desc(out, layout), _grid(grid), _ptr(idx), _ptr(count), cap,
+                                  _stream(stream))
+    _check(st, "bc_sparse_maxpool2d")
+
+
+def _np_ptr(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def bc_fold_bn(w, conv_bias, gamma, beta, mean, var, eps=1e-5):
+    """Host: fold inference batch norm into fp32 weights [cout, ...]; returns (w', b')."""
+    w = np.ascontiguousarray(w, np.float32)
+    cout = w.shape[0]
+    f = lambda a: None if a is None else np.ascontiguousarray(a, np.float32)
+    cb, g, b, m, v = f(conv_bias), f(gamma), f(beta), f(mean), f(var)
+    w_out = np.empty_like(w)
+    b_out = np.empty(cout, np.float32)
+    st = _lib.bc_fold_bn(_np_ptr(w), cout, int(w.size // cout), _np_ptr(cb), _np_ptr(g), _np_ptr(b),
+                         _np_ptr(m), _np_ptr(v), float(eps), _np_ptr(w_out), _np_ptr(b_out))
+    _check(st, "bc_fold_bn")
+    return w_out, b_out
+
+
+def bc_repack_weights(w_oihw, dtype_code):
+    """Host: fp32 OIHW -> [cout][kh][kw][cin] in the given dtype (numpy, raw bits for 16-bit)."""
+    w = np.ascontiguousarray(w_oihw, np.float32)
+    co, ci, kh, kw = w.shape
+    out = np.empty((co, kh, kw, ci), np.float32 if dtype_code == BC_F32 else np.uint16)
+    st = _lib.bc_repack_weights(_np_ptr(w), co, ci, kh, kw, int(dtype_code), _np_ptr(out))
+    _check(st, "bc_repack_weights")
+    return out
+
+
+class Buffer:
+    """A registered persistent buffer (wraps caller memory; see bc_buffer_* in bc.h)."""
+
+    def __init__(self, t, layout):
+        self.t = t
+        self.layout = layout
+        h = ctypes.c_void_p()
+        _check(_lib.bc_buffer_register(_ptr(t), desc(t, layout), ctypes.byref(h)), "bc_buffer_register")
+        self.handle = h
+
+    def release(self):
+        if self.handle is not None:
+            _check(_lib.bc_buffer_release(self.handle), "bc_buffer_release")
+            self.handle = None
+
+    def invalidate(self):
+        _check(_lib.bc_buffer_invalidate(self.handle), "bc_buffer_invalidate")
+
+    def mark_written(self, full_mask: bool):
+        _check(_lib.bc_buffer_mark_written(self.handle, int(bool(full_mask))), "bc_buffer_mark_written")
+
+    @property
+    def valid(self) -> int:
+        return int(_lib.bc_buffer_is_valid(self.handle))
+
+    def __del__(self):
+        try:
+            self.release()
+        except Exception:
+            pass
+
+
+def bc_buffer_register(t, layout) -> Buffer:
+    return Buffer(t, layout)
+
+
+def raw():
+    """The ctypes library object (for tests that call entry points with raw pointers)."""
+    return _lib

@@ -1,0 +1,504 @@
+// C-ABI layer of libblockcopy: argument validation, status codes, thread-local
+// error text, the persistent-buffer registry and kernel dispatch. Every check runs
+// before anything is enqueued; kernels are launched on the caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <set>
+#include <string>
+
+#include "../../include/bc.h"
+#include "bc_internal.h"
+
+using bc::LayerGeom;
+
+namespace {
+
+thread_local std::string g_err;
+
+bc_status fail(bc_status s, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+bc_status ok()
+{
+    g_err.clear();
+    return BC_OK;
+}
+
+bc_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(BC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int esize_of(int32_t dtype) { return dtype == BC_F32 ? 4 : 2; }
+
+bool valid_dtype(int32_t d) { return d == BC_F32 || d == BC_BF16 || d == BC_F16; }
+bool valid_layout(int32_t l) { return l == BC_NCHW || l == BC_NHWC; }
+
+size_t tensor_bytes(const bc_tensor &t)
+{
+    return (size_t)t.n * t.c * t.h * t.w * esize_of(t.dtype);
+}
+
+bc_status check_tensor(const bc_tensor &t, const char *name)
+{
+    if (t.n <= 0 || t.c <= 0 || t.h <= 0 || t.w <= 0)
+        return fail(BC_ERR_SHAPE, "%s: all sizes must be positive (n=%d c=%d h=%d w=%d)", name,
+                    t.n, t.c, t.h, t.w);
+    if (!valid_dtype(t.dtype)) return fail(BC_ERR_DTYPE, "%s: unknown dtype %d", name, t.dtype);
+    if (!valid_layout(t.layout)) return fail(BC_ERR_LAYOUT, "%s: unknown layout %d", name, t.layout);
+    if ((double)t.n * t.c * t.h * t.w > 4.0e9)
+        return fail(BC_ERR_SHAPE, "%s: more than 4e9 elements", name);
+    return BC_OK;
+}
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb)
+{
+    if (!a || !b || !na || !nb) return false;
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+// index arguments: both NULL = every block; otherwise both required + capacity
+bc_status check_index(const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                      int total_blocks)
+{
+    if ((d_idx == nullptr) != (d_count == nullptr))
+        return fail(BC_ERR_NULL, "d_idx and d_count must both be given or both be NULL");
+    if (d_idx && capacity < total_blocks)
+        return fail(BC_ERR_CAPACITY, "capacity %d < n*grid_h*grid_w = %d", capacity, total_blocks);
+    return BC_OK;
+}
+
+// Output blocks of `out` on grid g.
+bc_status block_geom(const bc_tensor &out, bc_grid g, LayerGeom &L)
+{
+    if (g.grid_h <= 0 || g.grid_w <= 0)
+        return fail(BC_ERR_SHAPE, "grid must be positive (%d x %d)", g.grid_h, g.grid_w);
+    if (out.h % g.grid_h || out.w % g.grid_w)
+        return fail(BC_ERR_NOT_DIVISIBLE, "output %d x %d not divisible by the %d x %d block grid",
+                    out.h, out.w, g.grid_h, g.grid_w);
+    if ((double)out.n * g.grid_h * g.grid_w > (double)(1 << 20))
+        return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    L.gh = g.grid_h;
+    L.gw = g.grid_w;
+    L.bh = out.h / g.grid_h;
+    L.bw = out.w / g.grid_w;
+    L.total_blocks = out.n * g.grid_h * g.grid_w;
+    return BC_OK;
+}
+
+bc_status check_geom(const bc_conv *c, bool conv)
+{
+    if (c->kh < 1 || c->kw < 1 || c->stride < 1 || c->pad < 0)
+        return fail(BC_ERR_SHAPE, "kernel %dx%d, stride %d, pad %d: kernel and stride must be "
+                                  ">= 1, pad >= 0", c->kh, c->kw, c->stride, c->pad);
+    if (conv && c->relu != 0 && c->relu != 1) return fail(BC_ERR_SHAPE, "relu must be 0 or 1");
+    return BC_OK;
+}
+
+int conv_out(int in, int k, int s, int p) { return in + 2 * p - k < 0 ? 0 : (in + 2 * p - k) / s + 1; }
+
+// ---------------------------------------------------------------- buffer registry
+
+std::mutex g_mu;
+std::set<bc_buffer> g_buffers;
+std::map<uintptr_t, bc_buffer> g_by_addr;
+
+}  // namespace
+
+struct bc_buffer_s {
+    void *mem;
+    bc_tensor desc;
+    size_t bytes;
+    int valid;
+};
+
+namespace {
+
+// Registered buffer that starts at d_out (nullptr if none).
+bc_buffer lookup_locked(const void *d_out)
+{
+    auto it = g_by_addr.find((uintptr_t)d_out);
+    return it == g_by_addr.end() ? nullptr : it->second;
+}
+
+bc_status check_registered(const void *d_out, const bc_tensor &out, bool sparse)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    bc_buffer b = lookup_locked(d_out);
+    if (!b) return BC_OK;
+    if (memcmp(&b->desc, &out, sizeof out) != 0)
+        return fail(BC_ERR_SHAPE, "output descriptor differs from the registered buffer's");
+    if (sparse && !b->valid)
+        return fail(BC_ERR_UNINITIALIZED,
+                    "sparse write into a registered buffer that holds no complete frame yet "
+                    "(run a full frame first)");
+    return BC_OK;
+}
+
+void mark_full(const void *d_out)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    bc_buffer b = lookup_locked(d_out);
+    if (b) b->valid = 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t bc_abi_version(void) { return BC_ABI_VERSION; }
+
+const char *bc_status_str(int32_t s)
+{
+    switch (s) {
+    case BC_OK: return "ok";
+    case BC_ERR_NULL: return "null pointer";
+    case BC_ERR_SHAPE: return "inconsistent shape";
+    case BC_ERR_DTYPE: return "dtype mismatch";
+    case BC_ERR_LAYOUT: return "layout mismatch";
+    case BC_ERR_NOT_DIVISIBLE: return "size not divisible by the block grid";
+    case BC_ERR_CAPACITY: return "capacity too small";
+    case BC_ERR_ALIAS: return "output overlaps an input";
+    case BC_ERR_UNINITIALIZED: return "sparse write into an invalid buffer";
+    case BC_ERR_UNSUPPORTED: return "unsupported configuration";
+    case BC_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+const char *bc_last_error(void) { return g_err.c_str(); }
+
+bc_status bc_build_block_index(const uint8_t *d_mask, int32_t n, bc_grid g, int32_t *d_idx,
+                               int32_t capacity, int32_t *d_count, int32_t *h_count,
+                               void *stream)
+{
+    if (!d_mask || !d_idx || !d_count) return fail(BC_ERR_NULL, "d_mask, d_idx and d_count are required");
+    if (n <= 0 || g.grid_h <= 0 || g.grid_w <= 0)
+        return fail(BC_ERR_SHAPE, "n and grid must be positive");
+    const double total = (double)n * g.grid_h * g.grid_w;
+    if (total > (double)(1 << 20)) return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    if (capacity < (int)total)
+        return fail(BC_ERR_CAPACITY, "capacity %d < n*grid_h*grid_w = %d", capacity, (int)total);
+    if (overlap(d_idx, (size_t)capacity * 4, d_count, 4) ||
+        overlap(d_mask, (size_t)total, d_idx, (size_t)capacity * 4) ||
+        overlap(d_mask, (size_t)total, d_count, 4))
+        return fail(BC_ERR_ALIAS, "mask, index and count must not overlap");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = bc::launch_block_index(d_mask, (int)total, d_idx, d_count, s);
+    if (e != hipSuccess) return hip_fail(e, "block index launch");
+    if (h_count) {
+        e = hipMemcpyAsync(h_count, d_count, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "count copy");
+    }
+    return ok();
+}
+
+static bc_status gs_common(const bc_tensor &t, bc_grid g, const bc_conv *geom, bool gather,
+                           const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                           LayerGeom &L)
+{
+    bc_status st = check_tensor(t, gather ? "src" : "dst");
+    if (st) return st;
+    if (gather) {
+        if (!geom) return fail(BC_ERR_NULL, "geom is required");
+        if ((st = check_geom(geom, false))) return st;
+        if (geom->stride > 2 || geom->kh > 7 || geom->kw > 7)
+            return fail(BC_ERR_UNSUPPORTED, "gather: stride must be 1 or 2 and kernel edges <= 7");
+        bc_tensor out = t;
+        out.h = conv_out(t.h, geom->kh, geom->stride, geom->pad);
+        out.w = conv_out(t.w, geom->kw, geom->stride, geom->pad);
+        if (out.h <= 0 || out.w <= 0) return fail(BC_ERR_SHAPE, "geometry gives an empty output");
+        if ((st = block_geom(out, g, L))) return st;
+        L.n = t.n; L.cin = t.c; L.hin = t.h; L.win = t.w;
+        L.cout = t.c; L.hout = out.h; L.wout = out.w;
+        L.kh = geom->kh; L.kw = geom->kw; L.stride = geom->stride; L.pad = geom->pad;
+    } else {
+        if ((st = block_geom(t, g, L))) return st;
+        L.n = t.n; L.cin = L.cout = t.c; L.hin = L.hout = t.h; L.win = L.wout = t.w;
+        L.kh = L.kw = L.stride = 1; L.pad = 0;
+    }
+    if ((st = check_index(d_idx, d_count, capacity, L.total_blocks))) return st;
+    L.idx = d_idx;
+    L.count = d_count;
+    return BC_OK;
+}
+
+static int packed_capacity(const int32_t *d_idx, int32_t capacity, int total)
+{
+    return d_idx ? capacity : total;
+}
+
+bc_status bc_gather_halo(const void *d_src, bc_tensor src, bc_grid g, const bc_conv *geom,
+                         float pad_value, const int32_t *d_idx, const int32_t *d_count,
+                         int32_t capacity, void *d_packed, void *stream)
+{
+    if (!d_src || !d_packed) return fail(BC_ERR_NULL, "d_src and d_packed are required");
+    LayerGeom L;
+    bc_status st = gs_common(src, g, geom, true, d_idx, d_count, capacity, L);
+    if (st) return st;
+    const int es = esize_of(src.dtype);
+    const size_t th = (size_t)(L.bh - 1) * L.stride + L.kh, tw = (size_t)(L.bw - 1) * L.stride + L.kw;
+    const size_t packed_bytes =
+        (size_t)packed_capacity(d_idx, capacity, L.total_blocks) * th * tw * src.c * es;
+    if (overlap(d_packed, packed_bytes, d_src, tensor_bytes(src)))
+        return fail(BC_ERR_ALIAS, "d_packed overlaps d_src");
+    uint32_t bits;
+    if (src.dtype == BC_F32) {
+        memcpy(&bits, &pad_value, 4);
+    } else if (src.dtype == BC_BF16) {
+        uint32_t u;
+        memcpy(&u, &pad_value, 4);
+        if ((u & 0x7FFFFFFFu) > 0x7F800000u) bits = (u >> 16) | 0x40u;
+        else bits = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    } else {
+        _Float16 h = (_Float16)pad_value;
+        uint16_t hb;
+        memcpy(&hb, &h, 2);
+        bits = hb;
+    }
+    hipError_t e = bc::launch_gather_halo(d_src, es, src.layout == BC_NHWC, L, bits, d_packed,
+                                          (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+    return ok();
+}
+
+bc_status bc_scatter_blocks(const void *d_packed, const int32_t *d_idx, const int32_t *d_count,
+                            int32_t capacity, bc_grid g, void *d_dst, bc_tensor dst, void *stream)
+{
+    if (!d_packed || !d_dst) return fail(BC_ERR_NULL, "d_packed and d_dst are required");
+    LayerGeom L;
+    bc_status st = gs_common(dst, g, nullptr, false, d_idx, d_count, capacity, L);
+    if (st) return st;
+    const int es = esize_of(dst.dtype);
+    const size_t packed_bytes = (size_t)packed_capacity(d_idx, capacity, L.total_blocks) * L.bh *
+                                L.bw * dst.c * es;
+    if (overlap(d_packed, packed_bytes, d_dst, tensor_bytes(dst)))
+        return fail(BC_ERR_ALIAS, "d_dst overlaps d_packed");
+    if (d_idx && overlap(d_dst, tensor_bytes(dst), d_idx, (size_t)capacity * 4))
+        return fail(BC_ERR_ALIAS, "d_dst overlaps the index");
+    hipError_t e = bc::launch_scatter_blocks(d_packed, es, dst.layout == BC_NHWC, L, d_dst,
+                                             (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "scatter launch");
+    return ok();
+}
+
+// Validation shared by the conv and pooling layers.
+static bc_status layer_common(const bc_conv *geom, bool conv, const void *d_in, const bc_tensor &in,
+                              void *d_out, const bc_tensor &out, bc_grid g, const int32_t *d_idx,
+                              const int32_t *d_count, int32_t capacity, LayerGeom &L)
+{
+    if (!geom || !d_in || !d_out) return fail(BC_ERR_NULL, "geometry, d_in and d_out are required");
+    bc_status st;
+    if ((st = check_geom(geom, conv))) return st;
+    if ((st = check_tensor(in, "in"))) return st;
+    if ((st = check_tensor(out, "out"))) return st;
+    if (in.dtype != out.dtype) return fail(BC_ERR_DTYPE, "in and out dtypes differ");
+    if (in.layout != out.layout) return fail(BC_ERR_LAYOUT, "in and out layouts differ");
+    if (in.layout == BC_NHWC && in.dtype == BC_F32)
+        return fail(BC_ERR_UNSUPPORTED, "channels-last layers take BF16 or F16");
+    if (in.layout == BC_NCHW && in.dtype != BC_F32)
+        return fail(BC_ERR_UNSUPPORTED, "channels-first layers take F32");
+    if (out.n != in.n) return fail(BC_ERR_SHAPE, "out.n %d != in.n %d", out.n, in.n);
+    const int oh = conv_out(in.h, geom->kh, geom->stride, geom->pad);
+    const int ow = conv_out(in.w, geom->kw, geom->stride, geom->pad);
+    if (out.h != oh || out.w != ow)
+        return fail(BC_ERR_SHAPE, "out is %dx%d but the geometry gives %dx%d", out.h, out.w, oh, ow);
+    if ((st = block_geom(out, g, L))) return st;
+    if ((st = check_index(d_idx, d_count, capacity, L.total_blocks))) return st;
+    if (overlap(d_out, tensor_bytes(out), d_in, tensor_bytes(in)))
+        return fail(BC_ERR_ALIAS, "d_out overlaps d_in");
+    if (d_idx && (overlap(d_out, tensor_bytes(out), d_idx, (size_t)capacity * 4) ||
+                  overlap(d_out, tensor_bytes(out), d_count, 4)))
+        return fail(BC_ERR_ALIAS, "d_out overlaps the index");
+    L.n = in.n; L.cin = in.c; L.hin = in.h; L.win = in.w;
+    L.cout = out.c; L.hout = out.h; L.wout = out.w;
+    L.kh = geom->kh; L.kw = geom->kw; L.stride = geom->stride; L.pad = geom->pad;
+    L.idx = d_idx;
+    L.count = d_count;
+    return BC_OK;
+}
+
+bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, const void *d_w,
+                           const float *d_bias, const void *d_residual, void *d_out, bc_tensor out,
+                           bc_grid g, const int32_t *d_idx, const int32_t *d_count,
+                           int32_t capacity, void *stream)
+{
+    if (!d_w) return fail(BC_ERR_NULL, "d_w is required");
+    LayerGeom L;
+    bc_status st = layer_common(conv, true, d_in, in, d_out, out, g, d_idx, d_count, capacity, L);
+    if (st) return st;
+    const size_t wbytes = (size_t)out.c * in.c * conv->kh * conv->kw * esize_of(in.dtype);
+    const size_t obytes = tensor_bytes(out);
+    if (overlap(d_out, obytes, d_w, wbytes)) return fail(BC_ERR_ALIAS, "d_out overlaps d_w");
+    if (overlap(d_out, obytes, d_residual, obytes)) return fail(BC_ERR_ALIAS, "d_out overlaps d_residual");
+    if (overlap(d_out, obytes, d_bias, (size_t)out.c * 4)) return fail(BC_ERR_ALIAS, "d_out overlaps d_bias");
+    const char *why = "";
+    if (in.layout == BC_NHWC) {
+        if (!bc::conv_nhwc_mfma_supported(L, &why)) return fail(BC_ERR_UNSUPPORTED, "%s", why);
+    } else {
+        const int th = (L.bh - 1) * L.stride + L.kh, tw = (L.bw - 1) * L.stride + L.kw;
+        if (L.bh * L.bw > 2048 || (th * tw + L.kh * L.kw) * 4 > 48 * 1024)
+            return fail(BC_ERR_UNSUPPORTED, "fp32 path: output blocks above 2048 pixels or halo "
+                                            "tiles above 48 KB per channel");
+    }
+    if ((st = check_registered(d_out, out, d_idx != nullptr))) return st;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (in.layout == BC_NHWC) {
+        e = bc::launch_conv_nhwc_mfma((const uint16_t *)d_in, (const uint16_t *)d_w, d_bias,
+                                      (const uint16_t *)d_residual, (uint16_t *)d_out, conv->relu,
+                                      in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16, L,
+                                      s, &why);
+    } else {
+        e = bc::launch_conv_nchw_f32((const float *)d_in, (const float *)d_w, d_bias,
+                                     (const float *)d_residual, (float *)d_out, conv->relu, L, s,
+                                     &why);
+    }
+    if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
+    if (e != hipSuccess) return hip_fail(e, "conv launch");
+    if (!d_idx) mark_full(d_out);
+    return ok();
+}
+
+bc_status bc_sparse_maxpool2d(const bc_conv *geom, const void *d_in, bc_tensor in, void *d_out,
+                              bc_tensor out, bc_grid g, const int32_t *d_idx,
+                              const int32_t *d_count, int32_t capacity, void *stream)
+{
+    LayerGeom L;
+    bc_status st = layer_common(geom, false, d_in, in, d_out, out, g, d_idx, d_count, capacity, L);
+    if (st) return st;
+    if (in.c != out.c) return fail(BC_ERR_SHAPE, "pooling keeps the channel count");
+    if (in.layout == BC_NHWC && in.c % 8)
+        return fail(BC_ERR_UNSUPPORTED, "channels-last pooling needs C % 8 == 0");
+    if ((st = check_registered(d_out, out, d_idx != nullptr))) return st;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (in.layout == BC_NHWC)
+        e = bc::launch_maxpool_nhwc16((const uint16_t *)d_in, (uint16_t *)d_out,
+                                      in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16, L, s);
+    else
+        e = bc::launch_maxpool_nchw32((const float *)d_in, (float *)d_out, L, s);
+    if (e != hipSuccess) return hip_fail(e, "maxpool launch");
+    if (!d_idx) mark_full(d_out);
+    return ok();
+}
+
+bc_status bc_fold_bn(const float *w, int32_t cout, int32_t per_out, const float *conv_bias,
+                     const float *gamma, const float *beta, const float *mean, const float *var,
+                     float eps, float *w_out, float *b_out)
+{
+    if (!w || !gamma || !beta || !mean || !var || !w_out || !b_out)
+        return fail(BC_ERR_NULL, "w, gamma, beta, mean, var, w_out and b_out are required");
+    if (cout <= 0 || per_out <= 0) return fail(BC_ERR_SHAPE, "cout and per_out must be positive");
+    for (int co = 0; co < cout; ++co) {
+        const double scale = (double)gamma[co] / sqrt((double)var[co] + (double)eps);
+        const double cb = conv_bias ? (double)conv_bias[co] : 0.0;
+        b_out[co] = (float)((double)beta[co] + (cb - (double)mean[co]) * scale);
+        for (int k = 0; k < per_out; ++k) {
+            const size_t i = (size_t)co * per_out + k;
+            w_out[i] = (float)((double)w[i] * scale);
+        }
+    }
+    return ok();
+}
+
+bc_status bc_repack_weights(const float *w_oihw, int32_t cout, int32_t cin, int32_t kh, int32_t kw,
+                            int32_t dtype, void *h_out)
+{
+    if (!w_oihw || !h_out) return fail(BC_ERR_NULL, "w_oihw and h_out are required");
+    if (cout <= 0 || cin <= 0 || kh <= 0 || kw <= 0) return fail(BC_ERR_SHAPE, "sizes must be positive");
+    if (!valid_dtype(dtype)) return fail(BC_ERR_DTYPE, "unknown dtype %d", dtype);
+    for (int co = 0; co < cout; ++co)
+        for (int i = 0; i < kh; ++i)
+            for (int j = 0; j < kw; ++j)
+                for (int ci = 0; ci < cin; ++ci) {
+                    const float v = w_oihw[(((size_t)co * cin + ci) * kh + i) * kw + j];
+                    const size_t o = (((size_t)co * kh + i) * kw + j) * cin + ci;
+                    if (dtype == BC_F32) {
+                        ((float *)h_out)[o] = v;
+                    } else if (dtype == BC_BF16) {
+                        uint32_t u;
+                        memcpy(&u, &v, 4);
+                        const uint32_t r = ((u & 0x7FFFFFFFu) > 0x7F800000u)
+                                               ? ((u >> 16) | 0x40u)
+                                               : ((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+                        ((uint16_t *)h_out)[o] = (uint16_t)r;
+                    } else {
+                        const _Float16 h = (_Float16)v;
+                        memcpy((uint16_t *)h_out + o, &h, 2);
+                    }
+                }
+    return ok();
+}
+
+bc_status bc_buffer_register(void *d_mem, bc_tensor desc, bc_buffer *out)
+{
+    if (!d_mem || !out) return fail(BC_ERR_NULL, "d_mem and out are required");
+    bc_status st = check_tensor(desc, "desc");
+    if (st) return st;
+    const size_t bytes = tensor_bytes(desc);
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (bc_buffer b : g_buffers)
+        if (overlap(b->mem, b->bytes, d_mem, bytes))
+            return fail(BC_ERR_ALIAS, "memory overlaps an already registered buffer");
+    bc_buffer b = new bc_buffer_s{d_mem, desc, bytes, 0};
+    g_buffers.insert(b);
+    g_by_addr[(uintptr_t)d_mem] = b;
+    *out = b;
+    return ok();
+}
+
+bc_status bc_buffer_release(bc_buffer b)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!b || !g_buffers.count(b)) return fail(BC_ERR_NULL, "unknown buffer handle");
+    g_by_addr.erase((uintptr_t)b->mem);
+    g_buffers.erase(b);
+    delete b;
+    return ok();
+}
+
+bc_status bc_buffer_invalidate(bc_buffer b)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!b || !g_buffers.count(b)) return fail(BC_ERR_NULL, "unknown buffer handle");
+    b->valid = 0;
+    return ok();
+}
+
+bc_status bc_buffer_mark_written(bc_buffer b, int32_t full_mask)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!b || !g_buffers.count(b)) return fail(BC_ERR_NULL, "unknown buffer handle");
+    if (full_mask) {
+        b->valid = 1;
+        return ok();
+    }
+    if (!b->valid)
+        return fail(BC_ERR_UNINITIALIZED, "sparse write recorded on a buffer with no full frame");
+    return ok();
+}
+
+int32_t bc_buffer_is_valid(bc_buffer b)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (!b || !g_buffers.count(b)) return -1;
+    return b->valid;
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// Internal declarations shared by the C-ABI layer (bc_api.cpp) and the HIP kernel
+// translation units. Not part of the public ABI (that is include/bc.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bc {
+
+// Geometry of one block-sparse layer call, resolved and validated on the host.
+// Output blocks are bh x bw pixels on a gh x gw grid per image; ids index them as
+// (img * gh + gy) * gw + gx. idx == nullptr means "every block" (full frame).
+struct LayerGeom {
+    int n, cin, hin, win;      // input
+    int cout, hout, wout;      // output
+    int kh, kw, stride, pad;
+    int gh, gw, bh, bw;
+    int total_blocks;          // n * gh * gw
+    const int32_t *idx;        // device, ascending active ids, or nullptr
+    const int32_t *count;      // device, number of active ids, or nullptr
+};
+
+// Storage formats of the half-width paths.
+enum class Half16 { BF16, F16 };
+
+hipError_t launch_block_index(const uint8_t *mask, int total, int32_t *idx, int32_t *count,
+                              hipStream_t s);
+
+// Gather/scatter of halo tiles, any element size (2 or 4 bytes), NHWC or NCHW source.
+hipError_t launch_gather_halo(const void *src, int esize, bool nhwc, const LayerGeom &g,
+                              uint32_t pad_bits, void *packed, hipStream_t s);
+hipError_t launch_scatter_blocks(const void *packed, int esize, bool nhwc, const LayerGeom &g,
+                                 void *dst, hipStream_t s);
+
+// Max pooling, NHWC bf16/f16 or NCHW f32.
+hipError_t launch_maxpool_nhwc16(const uint16_t *x, uint16_t *y, Half16 fmt, const LayerGeom &g,
+                                 hipStream_t s);
+hipError_t launch_maxpool_nchw32(const float *x, float *y, const LayerGeom &g, hipStream_t s);
+
+// Convolutions. Return hipErrorInvalidValue (with *why set) for shapes they cannot take.
+hipError_t launch_conv_nchw_f32(const float *x, const float *w, const float *bias,
+                                const float *res, float *y, int relu, const LayerGeom &g,
+                                hipStream_t s, const char **why);
+hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const float *bias,
+                                 const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
+                                 const LayerGeom &g, hipStream_t s, const char **why);
+// Host-side check used by the ABI validation before anything is enqueued.
+bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why);
+
+}  // namespace bc

@@ -1,0 +1,182 @@
+"""Frame-by-frame block-sparse ResNet backbones with persistent per-layer buffers.
+
+Single-stage networks make every convolution block-sparse (Section 4); all layers of
+a frame use the frame's one execution grid (Section 3.5); each layer's output is a
+persistent buffer that keeps transferred blocks from the previous execution
+(Section 3.1, Fig. 3); the first frame of a clip runs on every block (Section 4,
+BlockCopy configuration). Layers run in network order on one HIP stream.
+
+Backbones: ResNet-18 (basic blocks [2, 2, 2, 2]) and ResNet-50 (bottlenecks
+[3, 4, 6, 3], stride on the 3x3 convolution), 7x7/2 stem and 3x3/2 max pooling,
+batch norm folded into the convolutions (bc_fold_bn), no classifier. All feature
+maps are channels-last bf16 (or fp16). Work per frame: one bc_build_block_index and
+one library call per layer; nothing runs on the host in between.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import bc
+
+
+@dataclass
+class Layer:
+    kind: str                  # "conv" or "pool"
+    name: str
+    src: int                   # producing layer, -1 = the frame
+    cin: int
+    cout: int
+    k: int
+    stride: int
+    relu: bool = True
+    res: int | None = None     # layer whose buffer is added before the ReLU
+    params: dict = field(default_factory=dict)
+
+    @property
+    def pad(self) -> int:
+        return self.k // 2
+
+
+def build_layers(depth: int) -> list[Layer]:
+    """The backbone as a flat list in execution order."""
+    if depth == 18:
+        blocks, bottleneck = (2, 2, 2, 2), False
+    elif depth == 50:
+        blocks, bottleneck = (3, 4, 6, 3), True
+    else:
+        raise ValueError(f"ResNet-{depth} is not provided")
+    L = [Layer("conv", "stem", -1, 3, 64, 7, 2),
+         Layer("pool", "maxpool", 0, 64, 64, 3, 2, relu=False)]
+    cur, ch = 1, 64
+    for stage, nblk in enumerate(blocks):
+        width = 64 << stage
+        out_ch = width * (4 if bottleneck else 1)
+        for b in range(nblk):
+            stride = 2 if (stage and b == 0) else 1
+            tag = f"layer{stage + 1}.{b}"
+            shortcut = cur
+            if b == 0 and (stride != 1 or ch != out_ch):
+                L.append(Layer("conv", tag + ".downsample", cur, ch, out_ch, 1, stride, relu=False))
+                shortcut = len(L) - 1
+            if bottleneck:
+                L.append(Layer("conv", tag + ".conv1", cur, ch, width, 1, 1))
+                L.append(Layer("conv", tag + ".conv2", len(L) - 1, width, width, 3, stride))
+                L.append(Layer("conv", tag + ".conv3", len(L) - 1, width, out_ch, 1, 1, res=shortcut))
+            else:
+                L.append(Layer("conv", tag + ".conv1", cur, ch, width, 3, stride))
+                L.append(Layer("conv", tag + ".conv2", len(L) - 1, width, out_ch, 3, 1, res=shortcut))
+            cur, ch = len(L) - 1, out_ch
+    return L
+
+
+def default_params(layers: list[Layer], seed0: int = 1000, bn_random: bool = False):
+    """He-normal fp32 OIHW weights (seed seed0 + layer position) and batch-norm
+    statistics (identity unless bn_random), drawn by the shared input generators."""
+    import synth
+    out = []
+    for i, l in enumerate(layers):
+        if l.kind != "conv":
+            out.append(None)
+            continue
+        r = synth.rng(seed0 + i)
+        w = synth.he_normal(r, l.cout, l.cin, l.k, l.k)
+        c = l.cout
+        if bn_random:
+            bn = dict(gamma=r.uniform(0.5, 1.5, c), beta=r.normal(0, 0.1, c),
+                      mean=r.normal(0, 0.1, c), var=r.uniform(0.5, 1.5, c))
+        else:
+            bn = dict(gamma=np.ones(c), beta=np.zeros(c), mean=np.zeros(c), var=np.ones(c))
+        out.append(dict(w=w, **bn))
+    return out
+
+
+class SparseResNet:
+    """ResNet backbone executed block-sparsely frame by frame.
+
+    h, w: frame size; block: block edge in image pixels (the grid is h/block x
+    w/block for every layer, each layer's block edge is block / its stride).
+    """
+
+    def __init__(self, depth: int, h: int, w: int, block: int = 128, params=None,
+                 dtype=torch.bfloat16, device="cuda", seed0: int = 1000, bn_random: bool = False):
+        if h % block or w % block or block % 32:
+            raise ValueError("frame size must be a multiple of the block size, and the block "
+                             "size a multiple of 32 (the backbone's total stride)")
+        self.layers = build_layers(depth)
+        self.h, self.w, self.block = h, w, block
+        self.grid = (h // block, w // block)
+        self.dtype, self.device = dtype, torch.device(device)
+        dcode = bc.BC_BF16 if dtype == torch.bfloat16 else bc.BC_F16
+        params = params if params is not None else default_params(self.layers, seed0, bn_random)
+        self.shapes = []
+        for l in self.layers:
+            ih, iw = (h, w) if l.src < 0 else self.shapes[l.src][:2]
+            oh = (ih + 2 * l.pad - l.k) // l.stride + 1
+            ow = (iw + 2 * l.pad - l.k) // l.stride + 1
+            self.shapes.append((oh, ow, l.cout))
+        self.weights, self.biases = [], []
+        for l, p in zip(self.layers, params):
+            if l.kind != "conv":
+                self.weights.append(None)
+                self.biases.append(None)
+                continue
+            wf, bf = bc.bc_fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
+            wr = bc.bc_repack_weights(wf.reshape(p["w"].shape), dcode)
+            wt = torch.from_numpy(wr.view(np.int16)).view(dtype).to(self.device)
+            self.weights.append(wt.contiguous())
+            self.biases.append(torch.from_numpy(bf).to(self.device))
+        self.buffers = [torch.empty((1, oh, ow, c), dtype=dtype, device=self.device)
+                        for (oh, ow, c) in self.shapes]
+        self.handles = [bc.Buffer(t, bc.BC_NHWC) for t in self.buffers]
+        nblk = self.grid[0] * self.grid[1]
+        self.idx = torch.zeros(nblk, dtype=torch.int32, device=self.device)
+        self.count = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.mask = torch.zeros((1,) + self.grid, dtype=torch.uint8, device=self.device)
+
+    # ------------------------------------------------------------------
+    def conv_flops(self, active_blocks: int) -> float:
+        """Algorithmic FLOPs of the convolutions for one frame with that many active blocks."""
+        nblk = self.grid[0] * self.grid[1]
+        tot = 0.0
+        for l, (oh, ow, c) in zip(self.layers, self.shapes):
+            if l.kind == "conv":
+                tot += 2.0 * l.cin * l.cout * l.k * l.k * oh * ow * active_blocks / nblk
+        return tot
+
+    def invalidate(self):
+        """Start of a new clip: the next frame must be a full one."""
+        for hd in self.handles:
+            hd.invalidate()
+
+    def set_mask(self, mask):
+        """Copy an execution grid ([1, gh, gw] uint8, host or device) into the frame's mask."""
+        m = torch.as_tensor(np.asarray(mask, np.uint8) if not torch.is_tensor(mask) else mask)
+        self.mask.copy_(m.reshape(self.mask.shape), non_blocking=False)
+
+    def frame(self, x, sparse: bool = True, stream=None):
+        """Run one frame. x: [1, h, w, 3] channels-last on the device. sparse=False runs
+        every block (first frame of a clip); sparse=True uses the grid in self.mask."""
+        if sparse:
+            bc.bc_build_block_index(self.mask, 1, self.grid, self.idx, self.count, stream=stream)
+            idx, cnt = self.idx, self.count
+        else:
+            idx = cnt = None
+        for i, l in enumerate(self.layers):
+            self.run_layer(i, x, idx, cnt, stream)
+        return self.buffers[-1]
+
+    def run_layer(self, i, x, idx, cnt, stream=None):
+        l = self.layers[i]
+        src = x if l.src < 0 else self.buffers[l.src]
+        out = self.buffers[i]
+        if l.kind == "pool":
+            bc.bc_sparse_maxpool2d((l.k, l.k, l.stride, l.pad, 0), src, bc.BC_NHWC, out, self.grid,
+                                   idx, cnt, stream)
+        else:
+            res = None if l.res is None else self.buffers[l.res]
+            bc.bc_sparse_conv2d((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC,
+                                self.weights[i], self.biases[i], res, out, self.grid, idx, cnt,
+                                stream)
