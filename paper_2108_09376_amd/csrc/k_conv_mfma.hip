@@ -33,6 +33,10 @@
 // The stem form handles layers with few input channels (kw * Cin <= 32, e.g. the
 // 7x7 RGB stem): K is ordered (kernel row i, then the kw*Cin values of that row,
 // which are contiguous in a channels-last row), one MFMA k step per kernel row.
+#include <mutex>
+#include <set>
+#include <type_traits>
+
 #include "bc_internal.h"
 
 namespace bc {
@@ -42,6 +46,18 @@ typedef short short8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource: no swizzle, 32-bit dword data format; loads at offsets beyond
+// num_records return zeros instead of faulting.
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kOutOfRange = 0x7FFFFF00;     // byte offset past every buffer (< 2^31 - 256 bytes)
+
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int byte_off)
+{
+    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+    return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
 
 constexpr int kThreads = 256;
 constexpr int BK = 32;               // input channels per K step (one MFMA k)
@@ -60,6 +76,9 @@ struct MfmaArgs {
     int R, P, HR, HC, nslot, tpb, ntn;  // tiling: patch rows, patches/tile, patch rows/cols,
                                         // LDS slots, M tiles per block, N tiles
     int rowpitch;                       // stem form: elements per LDS halo row
+    float *ws;                          // split-K partial sums (pipelined form)
+    int x_bytes, w_bytes, y_bytes;      // buffer extents
+    int ksplit, cps;                    // K slices per tile, 32-channel chunks per slice
 };
 
 template <bool BF16>
@@ -93,109 +112,147 @@ __device__ __forceinline__ uint32_t to_h16(float z)
     }
 }
 
-// Active block of patch p of M tile mt; false when the patch lies beyond the count.
-__device__ __forceinline__ bool patch_block(const MfmaArgs &a, int count, int mt, int p,
-                                            int &img, int &oy0, int &ox0)
-{
-    int k, r0;
-    if (a.P == 1) {
-        k = mt / a.tpb;
-        r0 = (mt - k * a.tpb) * a.R;
-    } else {
-        k = mt * a.P + p;
-        r0 = 0;
-    }
-    if (k >= count) return false;
-    const int bid = a.idx ? a.idx[k] : k;
-    img = bid / (a.gh * a.gw);
-    const int rem = bid - img * a.gh * a.gw;
-    const int gy = rem / a.gw;
-    oy0 = gy * a.bh + r0;
-    ox0 = (rem - gy * a.gw) * a.bw;
-    return true;
-}
+// Blocks of one M tile, loaded once into LDS: patch p of the tile has output origin
+// (img, oy0, ox0); img < 0 marks a patch beyond the active count. Thread p < P loads
+// the active count and the block id in one round trip (ids are read unconditionally:
+// the index holds at least n*gh*gw entries). Returns false if the whole tile is
+// inactive (uniform across the workgroup).
+struct TileBlocks {
+    int img[16], oy0[16], ox0[16];
+    int live;
+};
 
-// Tile of this workgroup, XCD-first numbering over the T = mtiles * ntn live tiles.
-__device__ __forceinline__ bool tile_of(const MfmaArgs &a, int &count, int &mt, int &nt)
+__device__ __forceinline__ bool load_tile_blocks(const MfmaArgs &a, int mt, TileBlocks &tb)
 {
-    count = a.count ? *a.count : a.total_blocks;
-    const int mtiles = (a.P == 1) ? count * a.tpb : (count + a.P - 1) / a.P;
-    const int T = mtiles * a.ntn;
-    const int L = blockIdx.x;
-    if (L >= T) return false;
-    const int xcd = L & 7, j = L >> 3, q8 = T >> 3, r8 = T & 7;
-    const int logical = xcd * q8 + min(xcd, r8) + j;
-    mt = logical / a.ntn;
-    nt = logical - mt * a.ntn;
-    return true;
+    const int tid = threadIdx.x;
+    if (tid < a.P) {
+        const int cnt = a.count ? *a.count : a.total_blocks;
+        int k, r0;
+        if (a.P == 1) {
+            k = mt / a.tpb;
+            r0 = (mt - k * a.tpb) * a.R;
+        } else {
+            k = mt * a.P + tid;
+            r0 = 0;
+        }
+        int img = -1, oy0 = 0, ox0 = 0;
+        if (k < a.total_blocks) {
+            const int bid = a.idx ? a.idx[k] : k;
+            if (k < cnt) {
+                img = bid / (a.gh * a.gw);
+                const int rem = bid - img * a.gh * a.gw;
+                const int gy = rem / a.gw;
+                oy0 = gy * a.bh + r0;
+                ox0 = (rem - gy * a.gw) * a.bw;
+            }
+        }
+        tb.img[tid] = img;
+        tb.oy0[tid] = oy0;
+        tb.ox0[tid] = ox0;
+        if (tid == 0) tb.live = img >= 0;
+    }
+    __syncthreads();
+    return tb.live != 0;
 }
 
 // Fused epilogue: bias + residual + ReLU + rounding, 16-byte stores to block positions.
+// prefetch() runs before the main loop: it stages the tile's bias in LDS and requests
+// the residual of every output this lane will write, so those round trips overlap the
+// K loop. finish() transposes the fp32 accumulators through LDS (each lane then owns 8
+// consecutive channels of one pixel), adds bias and residual, applies ReLU, rounds to
+// the storage format and writes with 16-byte buffer stores; rows of inactive patches
+// use an out-of-range offset, which the hardware drops.
 template <bool BF16, int BM, int BN>
-__device__ __forceinline__ void epilogue(const MfmaArgs &a, f32x4 (&acc)[BM / 32][BN / 32],
-                                         uint8_t *smem, int count, int mt, int n0)
-{
-    constexpr int WM = BM / 2, WN = BN / 2, MI = WM / 16;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    float *scr = (float *)smem + wave * (WM * EPITCH);
-    const int rbw = a.R * a.bw;
+struct Epilogue {
+    static constexpr int WM = BM / 2, WN = BN / 2, MI = WM / 16;
+    static constexpr int NP = WN / 32, NU = WM / 16;
+    int rowoff[NU];            // byte offset of the output pixel of item u (kOutOfRange: none)
+    uint4 res[NP][NU];
+
+    __device__ __forceinline__ void prefetch(const MfmaArgs &a, const TileBlocks &tb, int n0,
+                                             float *s_bias)
+    {
+        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int wm = wave >> 1, wn = wave & 1;
+        for (int i = tid; i < BN; i += kThreads) s_bias[i] = a.bias ? a.bias[n0 + i] : 0.f;
+        const int rbw = a.R * a.bw;
 #pragma unroll
-    for (int np = 0; np < WN / 32; ++np) {
-        __syncthreads();
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-            for (int nn = 0; nn < 2; ++nn)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    scr[(mi * 16 + 4 * (lane >> 4) + i) * EPITCH + nn * 16 + (lane & 15)] =
-                        acc[mi][np * 2 + nn][i];
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < WM / 16; ++u) {
-            const int item = lane + 64 * u;
-            const int row = item >> 2, cv = item & 3;
-            const int m = wm * WM + row;
-            const int co = n0 + wn * WN + np * 32 + cv * 8;
+        for (int u = 0; u < NU; ++u) {
+            const int m = wm * WM + (lane >> 2) + 16 * u;
             const int p = m / rbw;
             const int local = m - p * rbw;
             const int pr = local / a.bw, pc = local - (local / a.bw) * a.bw;
-            int img, oy0, ox0;
-            if (!patch_block(a, count, mt, p, img, oy0, ox0)) continue;
-            const size_t pix = ((size_t)img * a.hout + oy0 + pr) * a.wout + ox0 + pc;
-            const float4 s0 = *(const float4 *)(scr + row * EPITCH + cv * 8);
-            const float4 s1 = *(const float4 *)(scr + row * EPITCH + cv * 8 + 4);
-            float z[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-            if (a.bias) {
-                const float4 b0 = *(const float4 *)(a.bias + co);
-                const float4 b1 = *(const float4 *)(a.bias + co + 4);
-                z[0] += b0.x; z[1] += b0.y; z[2] += b0.z; z[3] += b0.w;
-                z[4] += b1.x; z[5] += b1.y; z[6] += b1.z; z[7] += b1.w;
-            }
-            if (a.res) {
-                const uint4 r = *(const uint4 *)(a.res + pix * a.cout + co);
-                const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
+            const int img = tb.img[p];
+            rowoff[u] = img >= 0 ? (((img * a.hout + tb.oy0[p] + pr) * a.wout + tb.ox0[p] + pc) *
+                                    a.cout) * 2
+                                 : kOutOfRange;
+        }
+        if (a.res) {
+            const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)a.res, (short)0, a.y_bytes, kBufferFlags);
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    z[2 * t] += to_f32<BF16>(rw[t] & 0xFFFFu);
-                    z[2 * t + 1] += to_f32<BF16>(rw[t] >> 16);
-                }
-            }
-            uint32_t o[4];
+            for (int np = 0; np < NP; ++np) {
+                const int co = n0 + wn * WN + np * 32 + (lane & 3) * 8;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                float z0 = z[2 * t], z1 = z[2 * t + 1];
-                if (a.relu) {
-                    z0 = (z0 > 0.f || z0 != z0) ? z0 : 0.f;
-                    z1 = (z1 > 0.f || z1 != z1) ? z1 : 0.f;
-                }
-                o[t] = to_h16<BF16>(z0) | (to_h16<BF16>(z1) << 16);
+                for (int u = 0; u < NU; ++u)
+                    res[np][u] = bload(rr, rowoff[u] != kOutOfRange ? rowoff[u] + co * 2 : kOutOfRange);
             }
-            *(uint4 *)(a.y + pix * a.cout + co) = make_uint4(o[0], o[1], o[2], o[3]);
         }
     }
-}
+
+    __device__ __forceinline__ void finish(const MfmaArgs &a, f32x4 (&acc)[BM / 32][BN / 32],
+                                           uint8_t *smem, int n0, const float *s_bias)
+    {
+        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int wn = wave & 1;
+        float *scr = (float *)smem + wave * (WM * EPITCH);
+        const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)a.y, (short)0, a.y_bytes, kBufferFlags);
+#pragma unroll
+        for (int np = 0; np < NP; ++np) {
+            __syncthreads();
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int nn = 0; nn < 2; ++nn)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        scr[(mi * 16 + 4 * (lane >> 4) + i) * EPITCH + nn * 16 + (lane & 15)] =
+                            acc[mi][np * 2 + nn][i];
+            __syncthreads();
+            const int cl = wn * WN + np * 32 + (lane & 3) * 8;   // column within the tile
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int row = (lane >> 2) + 16 * u;
+                const float4 s0 = *(const float4 *)(scr + row * EPITCH + (lane & 3) * 8);
+                const float4 s1 = *(const float4 *)(scr + row * EPITCH + (lane & 3) * 8 + 4);
+                float z[8] = {s0.x + s_bias[cl], s0.y + s_bias[cl + 1], s0.z + s_bias[cl + 2],
+                              s0.w + s_bias[cl + 3], s1.x + s_bias[cl + 4], s1.y + s_bias[cl + 5],
+                              s1.z + s_bias[cl + 6], s1.w + s_bias[cl + 7]};
+                if (a.res) {
+                    const uint32_t rw[4] = {res[np][u].x, res[np][u].y, res[np][u].z, res[np][u].w};
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        z[2 * t] += to_f32<BF16>(rw[t] & 0xFFFFu);
+                        z[2 * t + 1] += to_f32<BF16>(rw[t] >> 16);
+                    }
+                }
+                i32x4 o;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    float z0 = z[2 * t], z1 = z[2 * t + 1];
+                    if (a.relu) {
+                        z0 = (z0 > 0.f || z0 != z0) ? z0 : 0.f;
+                        z1 = (z1 > 0.f || z1 != z1) ? z1 : 0.f;
+                    }
+                    o[t] = (int)(to_h16<BF16>(z0) | (to_h16<BF16>(z1) << 16));
+                }
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    o, yr, rowoff[u] != kOutOfRange ? rowoff[u] + (n0 + cl) * 2 : kOutOfRange, 0, 0);
+            }
+        }
+    }
+};
 
 // ------------------------------------------------------------------ general form
 
@@ -210,9 +267,13 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
     constexpr int BV = BN / 64;            // weight vectors per thread per K step
     extern __shared__ __align__(16) uint8_t smem[];
 
-    int count, mt, nt;
-    if (!tile_of(a, count, mt, nt)) return;
+    __shared__ TileBlocks tb;
+    __shared__ float s_bias[BN];
+    const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
+    if (!load_tile_blocks(a, mt, tb)) return;
+    Epilogue<BF16, BM, BN> epi;
+    epi.prefetch(a, tb, n0, s_bias);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int q = tid & 3;                 // 16-byte quarter of a 64-byte slot / weight row
@@ -230,9 +291,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
             const int p = slot / hrhc;
             const int r = slot - p * hrhc;
             const int ra = r / a.HC, rb = r - (r / a.HC) * a.HC;
-            int img, oy0, ox0;
-            if (patch_block(a, count, mt, p, img, oy0, ox0)) {
-                const int iy = oy0 * S - a.pad + ra * SS, ix = ox0 * S - a.pad + rb * SS;
+            const int img = tb.img[p];
+            if (img >= 0) {
+                const int iy = tb.oy0[p] * S - a.pad + ra * SS, ix = tb.ox0[p] * S - a.pad + rb * SS;
                 if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
                     aoff[u] = ((img * a.hin + iy) * a.win + ix) * a.cin;
             }
@@ -309,7 +370,262 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
                 for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
         }
     }
-    epilogue<BF16, BM, BN>(a, acc, smem, count, mt, n0);
+    epi.finish(a, acc, smem, n0, s_bias);
+}
+
+// ------------------------------------------------------------------ pipelined form (1x1, 3x3)
+//
+// The layers of ResNet backbones (1x1 and 3x3, stride 1 or 2) run here. At the
+// active fractions of sparse frames most layers have only a few workgroups per CU,
+// so time is set by how many dependent memory round trips a workgroup makes, not by
+// the matrix cores. This form therefore
+//  * loads the active count and the tile's block ids in one round trip (ids are
+//    read unconditionally; the index holds at least n*gh*gw entries);
+//  * keeps a D-deep ring of weight slices in registers: the slice of k step j+D is
+//    requested right after step j's slice is staged to LDS, so each request has D
+//    steps of matrix work to land (k step = one tap of one 32-channel chunk);
+//  * requests the next chunk's halo one chunk ahead (3x3: nine steps), or D steps
+//    ahead through its own register ring when every step is a new chunk (1x1);
+//  * splits K over `ksplit` workgroups for layers with few output tiles: each slice
+//    stores its fp32 partial tile, and the last slice to finish (a per-tile counter)
+//    adds the partials in fixed slice order 0, 1, ... and runs the epilogue, so the
+//    result does not depend on arrival order. The counter is reset by that last
+//    workgroup, so no memset is needed between calls (safe under graph replay).
+// LDS: halo double buffer + weight double buffer, one barrier per k step.
+
+constexpr int kMaxSplitTiles = 1 << 16;
+__device__ uint32_t g_split_counter[kMaxSplitTiles];   // zero at load, reset after use
+
+template <int BM, int KT>
+struct PipeShape {
+    static constexpr int AU = (KT == 1) ? BM / 64 : (BM == 64 ? 6 : 11);  // halo vectors / thread
+};
+
+template <bool BF16, int BM, int BN, int KS, int S, int D>
+__global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
+{
+    constexpr int SS = (KS == 1) ? S : 1;
+    constexpr int ST = S / SS;
+    constexpr int KT = KS * KS;
+    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int MI = WM / 16, NI = WN / 16;
+    constexpr int BV = BN / 64;
+    constexpr int AU = PipeShape<BM, KT>::AU;
+    extern __shared__ __align__(16) uint8_t smem[];
+    __shared__ TileBlocks tb;
+    __shared__ float s_bias[BN];
+    __shared__ int s_last;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1, q = tid & 3;
+    // natural tile order L = (mt * ntn + nt) * ksplit + ks: N tile and K slice are known
+    // without the active count
+    const int L = blockIdx.x;
+    const int ks = L % a.ksplit;
+    const int mn = L / a.ksplit;
+    const int nt = mn % a.ntn;
+    const int mt = mn / a.ntn;
+    const int n0 = nt * BN;
+    if (!load_tile_blocks(a, mt, tb)) return;   // tile beyond the active count (uniform)
+    Epilogue<BF16, BM, BN> epi;
+    epi.prefetch(a, tb, n0, s_bias);
+
+    const int nchunk = (a.cin + BK - 1) / BK;
+    const int c_lo = ks * a.cps;
+    const int c_hi = min(nchunk, c_lo + a.cps);
+    const int nsteps = (c_hi - c_lo) * KT;
+    const int hrhc = a.HR * a.HC;
+    const int aslot = ((a.nslot + 15) & ~15) * PITCH;
+    uint8_t *sA = smem;
+    uint8_t *sB = smem + 2 * aslot;
+
+    // Every request is issued unconditionally as a raw buffer load: lanes without data
+    // (zero padding, inactive patches, channels past Cin, steps past the slice) use an
+    // offset beyond the buffer, for which the hardware returns zeros. The loops below
+    // are therefore straight-line code and the compiler can wait for exactly the request
+    // a step needs instead of draining every outstanding one.
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
+    const int wq = ((n0 + (tid >> 2)) * KT * a.cin + q * 8) * 2;   // byte offset, tap 0 chunk 0
+    auto load_b = [&](int j, uint4 (&r)[BV]) {
+        const int c = c_lo + j / KT, tap = j - (j / KT) * KT;
+        const bool ok = j < nsteps && c * BK + q * 8 < a.cin;
+#pragma unroll
+        for (int v = 0; v < BV; ++v)
+            r[v] = bload(wr, ok ? wq + (64 * v * KT * a.cin + tap * a.cin + c * BK) * 2 : kOutOfRange);
+    };
+    // halo slot -> byte offset of its input pixel (kOutOfRange: zero padding / inactive patch)
+    int aoff[AU];
+#pragma unroll
+    for (int u = 0; u < AU; ++u) {
+        const int slot = (tid >> 2) + 64 * u;
+        aoff[u] = kOutOfRange;
+        if (slot < a.nslot) {
+            const int p = slot / hrhc;
+            const int r = slot - p * hrhc;
+            const int ra = r / a.HC, rb = r - (r / a.HC) * a.HC;
+            const int img = tb.img[p];
+            if (img >= 0) {
+                const int iy = tb.oy0[p] * S - a.pad + ra * SS;
+                const int ix = tb.ox0[p] * S - a.pad + rb * SS;
+                if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
+                    aoff[u] = (((img * a.hin + iy) * a.win + ix) * a.cin + q * 8) * 2;
+            }
+        }
+    }
+    auto load_a = [&](int c, uint4 (&r)[AU]) {
+        const bool ok = c < c_hi && c * BK + q * 8 < a.cin;
+#pragma unroll
+        for (int u = 0; u < AU; ++u)
+            r[u] = bload(xr, (ok && aoff[u] != kOutOfRange) ? aoff[u] + c * BK * 2 : kOutOfRange);
+    };
+    auto store_a = [&](uint8_t *sa, const uint4 (&r)[AU]) {
+#pragma unroll
+        for (int u = 0; u < AU; ++u) {
+            const int slot = (tid >> 2) + 64 * u;
+            if (slot < a.nslot) *(uint4 *)(sa + slot * PITCH + q * 16) = r[u];
+        }
+    };
+    auto store_b = [&](uint8_t *sb, const uint4 (&r)[BV]) {
+#pragma unroll
+        for (int v = 0; v < BV; ++v) *(uint4 *)(sb + ((tid >> 2) + 64 * v) * PITCH + q * 16) = r[v];
+    };
+    int abase[MI];
+    const int rbw = a.R * a.bw;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+        const int m = wm * WM + mi * 16 + (lane & 15);
+        const int p = m / rbw;
+        const int local = m - p * rbw;
+        const int pr = local / a.bw, pc = local - (local / a.bw) * a.bw;
+        abase[mi] = (p * hrhc + pr * ST * a.HC + pc * ST) * PITCH + (lane >> 4) * 16;
+    }
+    const int boff = (wn * WN + (lane & 15)) * PITCH + (lane >> 4) * 16;
+
+    f32x4 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](const uint8_t *sa, const uint8_t *sb, int toff) {
+        short8 af[MI], bf[NI];
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) af[mi] = *(const short8 *)(sa + abase[mi] + toff);
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) bf[ni] = *(const short8 *)(sb + boff + ni * 16 * PITCH);
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
+    };
+
+    if constexpr (KT == 1) {
+        // every k step is a new chunk: halo and weights ride D-deep register rings
+        uint4 rb[D][BV], ra[D][AU];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            load_b(d, rb[d]);
+            load_a(c_lo + d, ra[d]);
+        }
+        // ring slot d is a compile-time index in every step body
+        auto step = [&](auto dc, int j) {
+            constexpr int d = decltype(dc)::value;
+            uint8_t *sa = sA + (j & 1) * aslot;
+            uint8_t *sb = sB + (j & 1) * BN * PITCH;
+            store_a(sa, ra[d]);
+            store_b(sb, rb[d]);
+            __syncthreads();
+            load_b(j + D, rb[d]);
+            load_a(c_lo + j + D, ra[d]);
+            compute(sa, sb, 0);
+        };
+        static_assert(D == 4, "the step sequence below is written for four ring slots");
+        int j = 0;
+        for (; j + 4 <= nsteps; j += 4) {
+            step(std::integral_constant<int, 0>{}, j);
+            step(std::integral_constant<int, 1>{}, j + 1);
+            step(std::integral_constant<int, 2>{}, j + 2);
+            step(std::integral_constant<int, 3>{}, j + 3);
+        }
+        if (j < nsteps) step(std::integral_constant<int, 0>{}, j);
+        if (j + 1 < nsteps) step(std::integral_constant<int, 1>{}, j + 1);
+        if (j + 2 < nsteps) step(std::integral_constant<int, 2>{}, j + 2);
+    } else {
+        // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
+        // while the current chunk is multiplied
+        uint4 rb[KT][BV], ra[AU];
+#pragma unroll
+        for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
+        load_a(c_lo, ra);
+        const int nch = c_hi - c_lo;
+        for (int cj = 0; cj < nch; ++cj) {
+            uint8_t *sa = sA + (cj & 1) * aslot;
+            store_a(sa, ra);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) {
+                const int j = cj * KT + t;
+                uint8_t *sb = sB + (j & 1) * BN * PITCH;
+                store_b(sb, rb[t]);
+                __syncthreads();
+                load_b(j + KT, rb[t]);
+                if (t == 0) load_a(c_lo + cj + 1, ra);
+                compute(sa, sb, ((t / KS) * a.HC + (t % KS)) * PITCH);
+            }
+        }
+    }
+
+    if (a.ksplit > 1) {
+        // Hand the partial tile to the last slice. Partials are written through to the
+        // device-coherent level (agent-scope atomic stores), all of this workgroup's
+        // stores are waited for before the per-tile counter is incremented, and the last
+        // slice reads the others' partials with agent-scope loads, so no cache-wide
+        // write-back or invalidate is needed.
+        const int tile = mt * a.ntn + nt;
+        float *base = a.ws + (size_t)tile * a.ksplit * (BM * BN);
+        float *mine = base + (size_t)ks * (BM * BN);
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    __hip_atomic_store(mine + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4 + i,
+                                       acc[mi][ni][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (tid == 0)
+            s_last = __hip_atomic_fetch_add(&g_split_counter[tile], 1u, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(a.ksplit - 1);
+        __syncthreads();
+        if (!s_last) return;
+        f32x4 tot[MI][NI];
+        for (int sl = 0; sl < a.ksplit; ++sl) {
+            const float *src = base + (size_t)sl * (BM * BN);
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) {
+                    f32x4 v = acc[mi][ni];
+                    if (sl != ks) {
+                        const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            v[i] = __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    tot[mi][ni] = (sl == 0) ? v : tot[mi][ni] + v;   // fixed order 0, 1, 2, ...
+                }
+        }
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = tot[mi][ni];
+        if (tid == 0)
+            __hip_atomic_store(&g_split_counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    epi.finish(a, acc, smem, n0, s_bias);
 }
 
 // ------------------------------------------------------------------ stem form
@@ -322,9 +638,13 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
     constexpr int BKP = 40;  // elements per LDS weight row (32 + 8 pad)
     extern __shared__ __align__(16) uint8_t smem[];
 
-    int count, mt, nt;
-    if (!tile_of(a, count, mt, nt)) return;
+    __shared__ TileBlocks tb;
+    __shared__ float s_bias[BN];
+    const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
+    if (!load_tile_blocks(a, mt, tb)) return;
+    Epilogue<BF16, BM, BN> epi;
+    epi.prefetch(a, tb, n0, s_bias);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int kwc = KS * a.cin;            // values per kernel row, <= 32
@@ -339,10 +659,10 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
         const int row = e / rp, t = e - (e / rp) * rp;
         const int p = row / a.HR, ra = row - (row / a.HR) * a.HR;
         uint16_t v = 0;
-        int img, oy0, ox0;
-        if (t < rowvals && patch_block(a, count, mt, p, img, oy0, ox0)) {
+        const int img = tb.img[p];
+        if (t < rowvals && img >= 0) {
             const int rb = t / a.cin, ch = t - (t / a.cin) * a.cin;
-            const int iy = oy0 * S - a.pad + ra, ix = ox0 * S - a.pad + rb;
+            const int iy = tb.oy0[p] * S - a.pad + ra, ix = tb.ox0[p] * S - a.pad + rb;
             if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
                 v = a.x[(((size_t)img * a.hin + iy) * a.win + ix) * a.cin + ch];
         }
@@ -392,20 +712,27 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
     }
-    epilogue<BF16, BM, BN>(a, acc, smem, count, mt, n0);
+    epi.finish(a, acc, smem, n0, s_bias);
 }
 
 // ------------------------------------------------------------------ planning
 
+enum class Form { General, Stem, Pipe };
+
 struct Plan {
     int BM, BN;
-    bool stem;
+    Form form;
     MfmaArgs a;
     size_t lds;
+    size_t ws_bytes;
     unsigned grid;
 };
 
+constexpr int kPipeStages = 4;
+constexpr size_t kMaxLdsPipe = 160 * 1024;
+
 size_t epi_lds(int BM) { return (size_t)4 * (BM / 2) * EPITCH * sizeof(float); }
+size_t round16(size_t v) { return (v + 15) & ~(size_t)15; }
 
 // Tiling of the output blocks into M tiles of BM rows; false if BM cannot take them.
 bool tile_rows(const LayerGeom &g, int BM, MfmaArgs &a)
@@ -417,11 +744,14 @@ bool tile_rows(const LayerGeom &g, int BM, MfmaArgs &a)
     if (BM % (R * g.bw)) return false;
     const int P = BM / (R * g.bw);
     if (P > 1 && R != g.bh) return false;
+    if (P > 16) return false;
     a.R = R;
     a.P = P;
     a.tpb = (P == 1) ? g.bh / R : 1;
     return true;
 }
+
+int pipe_au(int BM, int KT) { return KT == 1 ? BM / 64 : (BM == 64 ? 6 : 11); }
 
 bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 {
@@ -429,8 +759,11 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
     if (g.cout % BN) return false;
     if (!tile_rows(g, BM, a)) return false;
     const int KS = g.kh, S = g.stride;
-    pl.stem = (g.cin % 8) != 0;
-    if (pl.stem) {
+    a.ksplit = 1;
+    a.cps = (g.cin + BK - 1) / BK;
+    pl.ws_bytes = 0;
+    if (g.cin % 8) {
+        pl.form = Form::Stem;
         if (KS * g.cin > 32 || BN != 64) return false;
         a.HR = (a.R - 1) * S + KS;
         a.HC = (g.bw - 1) * S + KS;
@@ -438,6 +771,7 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
         a.nslot = 0;
         const size_t main = (size_t)a.P * a.HR * a.rowpitch * 2 + (size_t)KS * BN * 40 * 2;
         pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+        if (pl.lds > kMaxLds) return false;
     } else {
         if (KS == 1) {
             a.HR = a.R;
@@ -447,12 +781,21 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
             a.HC = (g.bw - 1) * S + KS;
         }
         a.nslot = a.P * a.HR * a.HC;
-        if (a.nslot > 64 * kMaxAV) return false;
         a.rowpitch = 0;
-        const size_t main = (size_t)a.nslot * PITCH + (size_t)2 * BN * PITCH;
-        pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+        if (KS == 1 || KS == 3) {
+            pl.form = Form::Pipe;
+            if (a.nslot > 64 * pipe_au(BM, KS * KS)) return false;
+            const size_t main = 2 * round16(a.nslot) * PITCH + (size_t)2 * BN * PITCH;
+            pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+            if (pl.lds > kMaxLdsPipe) return false;
+        } else {
+            pl.form = Form::General;
+            if (a.nslot > 64 * kMaxAV) return false;
+            const size_t main = (size_t)a.nslot * PITCH + (size_t)2 * BN * PITCH;
+            pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+            if (pl.lds > kMaxLds) return false;
+        }
     }
-    if (pl.lds > kMaxLds) return false;
     pl.BM = BM;
     pl.BN = BN;
     a.ntn = g.cout / BN;
@@ -461,8 +804,11 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
     return true;
 }
 
-// Largest tiles that still give the full frame >= 1024 workgroups (about 300 at the
-// 30 % active fraction of the sparse frames), falling back to whatever fits.
+// Tiles: the largest that still give a full frame >= 2048 workgroups (about 600 at
+// 30 % of the blocks active), else the most workgroups. Pipelined layers that still
+// have fewer than 2048 tiles split K (at least 2 chunks per slice, at most 8 slices).
+// The choice depends on the layer's shape only, never on the active count, so an
+// active block's result does not depend on which other blocks are active.
 bool choose_plan(const LayerGeom &g, Plan &best)
 {
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
@@ -470,28 +816,93 @@ bool choose_plan(const LayerGeom &g, Plan &best)
     for (const auto &c : cand) {
         Plan p;
         if (!make_plan(g, c[0], c[1], p)) continue;
-        if (!have) {
+        if (!have || p.grid > best.grid) best = p;
+        have = true;
+        if (p.grid >= 2048) {
             best = p;
-            have = true;
+            break;
         }
-        if (p.grid >= 1024) {
-            best = p;
-            return true;
-        }
-        if (p.grid > best.grid) best = p;
     }
-    return have;
+    if (!have) return false;
+    if (best.form == Form::Pipe) {
+        MfmaArgs &a = best.a;
+        const int nchunk = (g.cin + BK - 1) / BK;
+        const unsigned tiles = best.grid;
+        int ks = 1;
+        while (ks < 8 && tiles * ks < 2048 && nchunk >= 4 * ks) ks *= 2;
+        a.cps = (nchunk + ks - 1) / ks;
+        a.ksplit = (nchunk + a.cps - 1) / a.cps;
+        if (a.ksplit > 1) {
+            if (tiles > (unsigned)kMaxSplitTiles) {
+                a.ksplit = 1;
+                a.cps = nchunk;
+            } else {
+                best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
+            }
+        }
+        best.grid = tiles * a.ksplit;
+    }
+    return true;
+}
+
+// Split-K workspace: one per device, grown on demand (never during a call that is
+// being captured into a graph if the first uncaptured call already sized it).
+std::mutex g_ws_mu;
+void *g_ws_ptr[64];
+size_t g_ws_bytes[64];
+
+hipError_t workspace(size_t bytes, float **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    if (g_ws_bytes[dev] < bytes) {
+        const size_t want = bytes < ((size_t)64 << 20) ? ((size_t)64 << 20) : bytes;
+        if (g_ws_ptr[dev]) {
+            e = hipFree(g_ws_ptr[dev]);
+            g_ws_ptr[dev] = nullptr;
+            g_ws_bytes[dev] = 0;
+            if (e != hipSuccess) return e;
+        }
+        e = hipMalloc(&g_ws_ptr[dev], want);
+        if (e != hipSuccess) {
+            g_ws_ptr[dev] = nullptr;
+            return e;
+        }
+        g_ws_bytes[dev] = want;
+    }
+    *out = (float *)g_ws_ptr[dev];
+    return hipSuccess;
+}
+
+std::mutex g_attr_mu;
+std::set<const void *> g_attr_done;
+
+template <typename K>
+void launch_kernel(K kernel, const Plan &p, hipStream_t s)
+{
+    if (p.lds > 64 * 1024) {
+        // opt in to more than 64 KB of LDS (gfx950 has 160 KB per workgroup), once per kernel
+        std::lock_guard<std::mutex> lk(g_attr_mu);
+        if (g_attr_done.insert((const void *)kernel).second)
+            (void)hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      (int)kMaxLdsPipe);
+    }
+    hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads), p.lds, s, p.a);
 }
 
 template <bool BF16, int BM, int BN, int KS, int S>
 void launch_one(const Plan &p, hipStream_t s)
 {
-    if (p.stem)
-        hipLaunchKernelGGL((k_conv_mfma_stem<BF16, BM, BN, KS, S>), dim3(p.grid), dim3(kThreads),
-                           p.lds, s, p.a);
-    else
-        hipLaunchKernelGGL((k_conv_mfma<BF16, BM, BN, KS, S>), dim3(p.grid), dim3(kThreads), p.lds,
-                           s, p.a);
+    if (p.form == Form::Stem) {
+        launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S>, p, s);
+    } else if (p.form == Form::Pipe) {
+        if constexpr (KS == 1 || KS == 3) launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, kPipeStages>, p, s);
+    } else {
+        launch_kernel(k_conv_mfma<BF16, BM, BN, KS, S>, p, s);
+    }
 }
 
 template <bool BF16, int KS, int S>
@@ -532,9 +943,10 @@ bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why)
         *why = "matrix-core path: Cin must be a multiple of 8, or kw*Cin <= 32 (stem form)";
         return false;
     }
-    if ((double)g.n * g.hin * g.win * g.cin >= 2147483647.0 ||
-        (double)g.cout * g.kh * g.kw * g.cin >= 2147483647.0) {
-        *why = "matrix-core path: tensor larger than 2^31 elements";
+    if (2.0 * g.n * g.hin * g.win * g.cin >= 2147483392.0 ||
+        2.0 * g.n * g.hout * g.wout * g.cout >= 2147483392.0 ||
+        2.0 * g.cout * g.kh * g.kw * g.cin >= 2147483392.0) {
+        *why = "matrix-core path: input, output or weight tensor of 2 GiB or more";
         return false;
     }
     Plan p;
@@ -560,7 +972,15 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     a.hout = g.hout; a.wout = g.wout; a.cout = g.cout;
     a.pad = g.pad; a.relu = relu;
     a.gh = g.gh; a.gw = g.gw; a.bh = g.bh; a.bw = g.bw; a.total_blocks = g.total_blocks;
+    a.ws = nullptr;
+    a.x_bytes = (int)((size_t)g.n * g.hin * g.win * g.cin * 2);
+    a.w_bytes = (int)((size_t)g.cout * g.kh * g.kw * g.cin * 2);
+    a.y_bytes = (int)((size_t)g.n * g.hout * g.wout * g.cout * 2);
     if (p.grid == 0) return hipSuccess;
+    if (p.ws_bytes) {
+        hipError_t e = workspace(p.ws_bytes, &a.ws);
+        if (e != hipSuccess) return e;
+    }
     if (fmt == Half16::BF16) launch_geom<true>(p, g.kh, g.stride, s);
     else launch_geom<false>(p, g.kh, g.stride, s);
     return hipGetLastError();
