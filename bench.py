@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only N plain steps (for rocprofv3) and print nothing else")
+    ap.add_argument("--rocprof-summary", metavar="KERNEL_STATS_CSV",
+                    help="print a text summary of a rocprofv3 --stats kernel table and exit")
     return ap.parse_args()
 
 
@@ -76,8 +78,33 @@ def cpu_baseline(mask):
                       f"{int((mask != 0).sum())}/{gh * gw} blocks active; {dt:.1f} s"}
 
 
+def rocprof_summary(path):
+    """Text summary of a rocprofv3 kernel_stats.csv: per-kernel calls / average / total,
+    and the sparse-conv kernels (k_conv_*) pooled into one average launch duration."""
+    import csv
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = [f"{'kernel':70s} {'calls':>7s} {'avg_us':>9s} {'total_ms':>9s} {'pct':>6s}"]
+    conv_n = conv_t = 0.0
+    for r in rows:
+        name = r["Name"].replace("(anonymous namespace)::", "")
+        name = name.split("(bc::")[0]
+        n, avg, tot = int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["TotalDurationNs"]) / 1e6
+        lines.append(f"{name[:70]:70s} {n:7d} {avg:9.2f} {tot:9.3f} {float(r['Percentage']):6.2f}")
+        if "k_conv_" in r["Name"]:
+            conv_n += n
+            conv_t += float(r["TotalDurationNs"])
+    if conv_n:
+        lines.append(f"sparse conv kernels pooled: {int(conv_n)} launches, average "
+                     f"{conv_t / conv_n / 1e3:.2f} us per launch")
+    return "\n".join(lines)
+
+
 def main():
     args = parse()
+    if args.rocprof_summary:
+        print(rocprof_summary(args.rocprof_summary))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -153,27 +180,35 @@ def main():
         sweep[f"{f:g}"] = round(time_frames(f, max(10, args.steps // 2), 3), 4)
     sweep[f"{args.frac:g}"] = round(ms, 4)
 
-    # Per-launch durations of the dominant kernel (sparse conv), HIP events on its stream.
+    # Per-launch durations of the dominant kernel (the sparse conv). Each conv layer is
+    # captured as a graph of `reps` back-to-back launches on the frame's index and timed
+    # with HIP events on the capture stream, so host-side marshalling is not counted.
     net.set_mask(mask)
-    nl = len(net.layers)
-    reps = max(5, args.steps // 5)
-    conv_ms = [0.0] * nl
-    for rep in range(reps + 2):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
-        from paper_2108_09376_amd import bc
-        bc.bc_build_block_index(net.mask, 1, net.grid, net.idx, net.count)
-        for i in range(nl):
-            ev[i][0].record()
-            net.run_layer(i, x, net.idx, net.count)
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        if rep >= 2:
-            for i in range(nl):
-                conv_ms[i] += ev[i][0].elapsed_time(ev[i][1]) / reps
+    from paper_2108_09376_amd import bc
+    bc.bc_build_block_index(net.mask, 1, net.grid, net.idx, net.count)
+    torch.cuda.synchronize()
     conv_idx = [i for i, l in enumerate(net.layers) if l.kind == "conv"]
-    conv_total_ms = sum(conv_ms[i] for i in conv_idx)
-    achieved = flops / (conv_total_ms * 1e-3) / 1e12
-    per_launch_us = conv_total_ms * 1e3 / len(conv_idx)
+    reps = 10
+    layer_us = {}
+    for i in conv_idx:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                net.run_layer(i, x, net.idx, net.count)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        layer_us[i] = e0.elapsed_time(e1) * 1e3 / (3 * reps)
+        del g
+    conv_total_us = sum(layer_us.values())
+    achieved = flops / (conv_total_us * 1e-6) / 1e12
+    per_launch_us = conv_total_us / len(conv_idx)
+    slowest = sorted(layer_us.items(), key=lambda kv: -kv[1])[:5]
 
     out = {
         "metric": "effective TFLOP/s on active blocks + ms/frame at 2048x1024, 30% active",
@@ -197,7 +232,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "sparse conv (k_conv_mfma*, all 53 launches of a frame)",
                      "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
-                     "avg_launch_us": round(per_launch_us, 3), "traffic": None},
+                     "avg_launch_us": round(per_launch_us, 3), "conv_us_per_frame": round(conv_total_us, 2),
+                     "traffic": None,
+                     "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mask)
