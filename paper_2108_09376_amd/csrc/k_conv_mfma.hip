@@ -66,6 +66,22 @@ constexpr int kMaxAV = 12;           // halo slots per thread quarter: nslot <= 
 constexpr int EPITCH = 36;           // floats per epilogue scratch row (32 + 4 pad)
 constexpr size_t kMaxLds = 64 * 1024;
 
+// Division by a per-launch constant d: q = umulhi(n, ceil(2^32 / d)), exact whenever
+// n * d < 2^32 (all uses here have n, d < 2^14); d = 1 is stored as m = 0.
+struct FastDiv {
+    uint32_t m;
+};
+
+__device__ __forceinline__ int fdiv(int n, FastDiv f)
+{
+    return f.m ? (int)__umulhi((uint32_t)n, f.m) : n;
+}
+
+FastDiv make_fastdiv(int d)
+{
+    return FastDiv{d == 1 ? 0u : (uint32_t)((((uint64_t)1 << 32) + (uint64_t)d - 1) / (uint64_t)d)};
+}
+
 struct MfmaArgs {
     const uint16_t *x, *w, *res;
     const float *bias;
@@ -78,7 +94,9 @@ struct MfmaArgs {
     int rowpitch;                       // stem form: elements per LDS halo row
     float *ws;                          // split-K partial sums (pipelined form)
     int x_bytes, w_bytes, y_bytes;      // buffer extents
+    FastDiv f_hrhc, f_hc, f_rbw, f_bw;  // divisions by HR*HC, HC, R*bw, bw
     int ksplit, cps;                    // K slices per tile, 32-channel chunks per slice
+    int tiles_full;                     // tiles (incl. K slices) of a full frame
 };
 
 template <bool BF16>
@@ -97,6 +115,22 @@ __device__ __forceinline__ float to_f32(uint32_t h)
 {
     if constexpr (BF16) return __uint_as_float(h << 16);
     else return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> two storage values packed in 32 bits (low = first), round to
+// nearest even; NaN stays NaN. bf16 uses the gfx950 packed conversion instruction.
+template <bool BF16>
+__device__ __forceinline__ uint32_t pack_h16(float z0, float z1)
+{
+    if constexpr (BF16) {
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{z0, z1}, bf16x2));
+    } else {
+        return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)z0) |
+               ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)z1) << 16);
+    }
 }
 
 // fp32 -> storage format, round to nearest even; NaN stays NaN.
@@ -156,9 +190,8 @@ __device__ __forceinline__ bool load_tile_blocks(const MfmaArgs &a, int mt, Tile
 }
 
 // Fused epilogue: bias + residual + ReLU + rounding, 16-byte stores to block positions.
-// prefetch() runs before the main loop: it stages the tile's bias in LDS and requests
-// the residual of every output this lane will write, so those round trips overlap the
-// K loop. finish() transposes the fp32 accumulators through LDS (each lane then owns 8
+// prefetch() runs before the main loop: it requests the bias and the residual of every
+// output this lane will write, so those round trips overlap the K loop. finish() transposes the fp32 accumulators through LDS (each lane then owns 8
 // consecutive channels of one pixel), adds bias and residual, applies ReLU, rounds to
 // the storage format and writes with 16-byte buffer stores; rows of inactive patches
 // use an out-of-range offset, which the hardware drops.
@@ -168,20 +201,28 @@ struct Epilogue {
     static constexpr int NP = WN / 32, NU = WM / 16;
     int rowoff[NU];            // byte offset of the output pixel of item u (kOutOfRange: none)
     uint4 res[NP][NU];
+    uint4 bias[NP][2];         // bias of this lane's 8 output channels per pass (fp32 bits)
 
-    __device__ __forceinline__ void prefetch(const MfmaArgs &a, const TileBlocks &tb, int n0,
-                                             float *s_bias)
+    __device__ __forceinline__ void prefetch(const MfmaArgs &a, const TileBlocks &tb, int n0)
     {
         const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
         const int wm = wave >> 1, wn = wave & 1;
-        for (int i = tid; i < BN; i += kThreads) s_bias[i] = a.bias ? a.bias[n0 + i] : 0.f;
+        // no bias: an empty buffer, every load returns zeros
+        const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)a.bias, (short)0, a.bias ? a.cout * 4 : 0, kBufferFlags);
+#pragma unroll
+        for (int np = 0; np < NP; ++np) {
+            const int co = n0 + wn * WN + np * 32 + (lane & 3) * 8;
+            bias[np][0] = bload(br, co * 4);
+            bias[np][1] = bload(br, co * 4 + 16);
+        }
         const int rbw = a.R * a.bw;
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
             const int m = wm * WM + (lane >> 2) + 16 * u;
-            const int p = m / rbw;
+            const int p = fdiv(m, a.f_rbw);
             const int local = m - p * rbw;
-            const int pr = local / a.bw, pc = local - (local / a.bw) * a.bw;
+            const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
             const int img = tb.img[p];
             rowoff[u] = img >= 0 ? (((img * a.hout + tb.oy0[p] + pr) * a.wout + tb.ox0[p] + pc) *
                                     a.cout) * 2
@@ -201,7 +242,7 @@ struct Epilogue {
     }
 
     __device__ __forceinline__ void finish(const MfmaArgs &a, f32x4 (&acc)[BM / 32][BN / 32],
-                                           uint8_t *smem, int n0, const float *s_bias)
+                                           uint8_t *smem, int n0)
     {
         const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
         const int wn = wave & 1;
@@ -226,9 +267,11 @@ struct Epilogue {
                 const int row = (lane >> 2) + 16 * u;
                 const float4 s0 = *(const float4 *)(scr + row * EPITCH + (lane & 3) * 8);
                 const float4 s1 = *(const float4 *)(scr + row * EPITCH + (lane & 3) * 8 + 4);
-                float z[8] = {s0.x + s_bias[cl], s0.y + s_bias[cl + 1], s0.z + s_bias[cl + 2],
-                              s0.w + s_bias[cl + 3], s1.x + s_bias[cl + 4], s1.y + s_bias[cl + 5],
-                              s1.z + s_bias[cl + 6], s1.w + s_bias[cl + 7]};
+                const uint4 b0 = bias[np][0], b1 = bias[np][1];
+                float z[8] = {s0.x + __uint_as_float(b0.x), s0.y + __uint_as_float(b0.y),
+                              s0.z + __uint_as_float(b0.z), s0.w + __uint_as_float(b0.w),
+                              s1.x + __uint_as_float(b1.x), s1.y + __uint_as_float(b1.y),
+                              s1.z + __uint_as_float(b1.z), s1.w + __uint_as_float(b1.w)};
                 if (a.res) {
                     const uint32_t rw[4] = {res[np][u].x, res[np][u].y, res[np][u].z, res[np][u].w};
 #pragma unroll
@@ -245,7 +288,7 @@ struct Epilogue {
                         z0 = (z0 > 0.f || z0 != z0) ? z0 : 0.f;
                         z1 = (z1 > 0.f || z1 != z1) ? z1 : 0.f;
                     }
-                    o[t] = (int)(to_h16<BF16>(z0) | (to_h16<BF16>(z1) << 16));
+                    o[t] = (int)pack_h16<BF16>(z0, z1);
                 }
                 __builtin_amdgcn_raw_buffer_store_b128(
                     o, yr, rowoff[u] != kOutOfRange ? rowoff[u] + (n0 + cl) * 2 : kOutOfRange, 0, 0);
@@ -268,12 +311,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
     extern __shared__ __align__(16) uint8_t smem[];
 
     __shared__ TileBlocks tb;
-    __shared__ float s_bias[BN];
     const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
     if (!load_tile_blocks(a, mt, tb)) return;
     Epilogue<BF16, BM, BN> epi;
-    epi.prefetch(a, tb, n0, s_bias);
+    epi.prefetch(a, tb, n0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int q = tid & 3;                 // 16-byte quarter of a 64-byte slot / weight row
@@ -370,7 +412,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
                 for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
         }
     }
-    epi.finish(a, acc, smem, n0, s_bias);
+    epi.finish(a, acc, smem, n0);
 }
 
 // ------------------------------------------------------------------ pipelined form (1x1, 3x3)
@@ -394,6 +436,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
 // LDS: halo double buffer + weight double buffer, one barrier per k step.
 
 constexpr int kMaxSplitTiles = 1 << 16;
+constexpr int kMaxSplit = 4;        // K slices per tile
 __device__ uint32_t g_split_counter[kMaxSplitTiles];   // zero at load, reset after use
 
 template <int BM, int KT>
@@ -413,7 +456,6 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     constexpr int AU = PipeShape<BM, KT>::AU;
     extern __shared__ __align__(16) uint8_t smem[];
     __shared__ TileBlocks tb;
-    __shared__ float s_bias[BN];
     __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -426,26 +468,18 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     const int nt = mn % a.ntn;
     const int mt = mn / a.ntn;
     const int n0 = nt * BN;
-    if (!load_tile_blocks(a, mt, tb)) return;   // tile beyond the active count (uniform)
-    Epilogue<BF16, BM, BN> epi;
-    epi.prefetch(a, tb, n0, s_bias);
-
     const int nchunk = (a.cin + BK - 1) / BK;
     const int c_lo = ks * a.cps;
     const int c_hi = min(nchunk, c_lo + a.cps);
     const int nsteps = (c_hi - c_lo) * KT;
-    const int hrhc = a.HR * a.HC;
-    const int aslot = ((a.nslot + 15) & ~15) * PITCH;
-    uint8_t *sA = smem;
-    uint8_t *sB = smem + 2 * aslot;
 
     // Every request is issued unconditionally as a raw buffer load: lanes without data
     // (zero padding, inactive patches, channels past Cin, steps past the slice) use an
     // offset beyond the buffer, for which the hardware returns zeros. The loops below
     // are therefore straight-line code and the compiler can wait for exactly the request
-    // a step needs instead of draining every outstanding one.
-    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
+    // a step needs instead of draining every outstanding one. Requests return in issue
+    // order, so they are issued in the order they are needed: halo, weights, epilogue.
+    if (!load_tile_blocks(a, mt, tb)) return;   // tile beyond the active count (uniform)
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
     const int wq = ((n0 + (tid >> 2)) * KT * a.cin + q * 8) * 2;   // byte offset, tap 0 chunk 0
@@ -456,6 +490,14 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
         for (int v = 0; v < BV; ++v)
             r[v] = bload(wr, ok ? wq + (64 * v * KT * a.cin + tap * a.cin + c * BK) * 2 : kOutOfRange);
     };
+    constexpr int RB = (KT == 1) ? D : KT;   // weight ring depth in k steps
+    const int hrhc = a.HR * a.HC;
+    const int aslot = ((a.nslot + 15) & ~15) * PITCH;
+    uint8_t *sA = smem;
+    uint8_t *sB = smem + 2 * aslot;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
+
     // halo slot -> byte offset of its input pixel (kOutOfRange: zero padding / inactive patch)
     int aoff[AU];
 #pragma unroll
@@ -463,13 +505,13 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
         const int slot = (tid >> 2) + 64 * u;
         aoff[u] = kOutOfRange;
         if (slot < a.nslot) {
-            const int p = slot / hrhc;
+            const int p = fdiv(slot, a.f_hrhc);
             const int r = slot - p * hrhc;
-            const int ra = r / a.HC, rb = r - (r / a.HC) * a.HC;
+            const int hy = fdiv(r, a.f_hc), hx = r - hy * a.HC;
             const int img = tb.img[p];
             if (img >= 0) {
-                const int iy = tb.oy0[p] * S - a.pad + ra * SS;
-                const int ix = tb.ox0[p] * S - a.pad + rb * SS;
+                const int iy = tb.oy0[p] * S - a.pad + hy * SS;
+                const int ix = tb.ox0[p] * S - a.pad + hx * SS;
                 if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
                     aoff[u] = (((img * a.hin + iy) * a.win + ix) * a.cin + q * 8) * 2;
             }
@@ -497,9 +539,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
         const int m = wm * WM + mi * 16 + (lane & 15);
-        const int p = m / rbw;
+        const int p = fdiv(m, a.f_rbw);
         const int local = m - p * rbw;
-        const int pr = local / a.bw, pc = local - (local / a.bw) * a.bw;
+        const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
         abase[mi] = (p * hrhc + pr * ST * a.HC + pc * ST) * PITCH + (lane >> 4) * 16;
     }
     const int boff = (wn * WN + (lane & 15)) * PITCH + (lane >> 4) * 16;
@@ -522,14 +564,17 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
             for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
     };
 
+    Epilogue<BF16, BM, BN> epi;
     if constexpr (KT == 1) {
         // every k step is a new chunk: halo and weights ride D-deep register rings
-        uint4 rb[D][BV], ra[D][AU];
+        uint4 ra[D][AU];
+        uint4 rb[RB][BV];
 #pragma unroll
         for (int d = 0; d < D; ++d) {
-            load_b(d, rb[d]);
             load_a(c_lo + d, ra[d]);
+            load_b(d, rb[d]);
         }
+        epi.prefetch(a, tb, n0);
         // ring slot d is a compile-time index in every step body
         auto step = [&](auto dc, int j) {
             constexpr int d = decltype(dc)::value;
@@ -556,10 +601,12 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     } else {
         // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
         // while the current chunk is multiplied
-        uint4 rb[KT][BV], ra[AU];
+        uint4 ra[AU];
+        uint4 rb[RB][BV];
+        load_a(c_lo, ra);
 #pragma unroll
         for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
-        load_a(c_lo, ra);
+        epi.prefetch(a, tb, n0);
         const int nch = c_hi - c_lo;
         for (int cj = 0; cj < nch; ++cj) {
             uint8_t *sa = sA + (cj & 1) * aslot;
@@ -577,7 +624,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
         }
     }
 
-    if (a.ksplit > 1) {
+    if constexpr (BM == 64 && BN == 64) if (a.ksplit > 1) {
         // Hand the partial tile to the last slice. Partials are written through to the
         // device-coherent level (agent-scope atomic stores), all of this workgroup's
         // stores are waited for before the per-tile counter is incremented, and the last
@@ -601,31 +648,37 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
                                             __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(a.ksplit - 1);
         __syncthreads();
         if (!s_last) return;
-        f32x4 tot[MI][NI];
-        for (int sl = 0; sl < a.ksplit; ++sl) {
+        // request every other slice's partial first, then add in slice order 0, 1, ...
+        f32x4 part[kMaxSplit][MI][NI];
+#pragma unroll
+        for (int sl = 0; sl < kMaxSplit; ++sl) {
+            if (sl >= a.ksplit || sl == ks) continue;
             const float *src = base + (size_t)sl * (BM * BN);
 #pragma unroll
             for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < NI; ++ni) {
-                    f32x4 v = acc[mi][ni];
-                    if (sl != ks) {
-                        const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
+                    const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
 #pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            v[i] = __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
-                    tot[mi][ni] = (sl == 0) ? v : tot[mi][ni] + v;   // fixed order 0, 1, 2, ...
+                    for (int i = 0; i < 4; ++i)
+                        part[sl][mi][ni][i] =
+                            __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
         }
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = tot[mi][ni];
+            for (int ni = 0; ni < NI; ++ni) {
+                f32x4 tot = (ks == 0) ? acc[mi][ni] : part[0][mi][ni];
+#pragma unroll
+                for (int sl = 1; sl < kMaxSplit; ++sl)
+                    if (sl < a.ksplit) tot += (sl == ks) ? acc[mi][ni] : part[sl][mi][ni];
+                acc[mi][ni] = tot;
+            }
         if (tid == 0)
             __hip_atomic_store(&g_split_counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    epi.finish(a, acc, smem, n0, s_bias);
+    epi.finish(a, acc, smem, n0);
 }
 
 // ------------------------------------------------------------------ stem form
@@ -639,12 +692,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
     extern __shared__ __align__(16) uint8_t smem[];
 
     __shared__ TileBlocks tb;
-    __shared__ float s_bias[BN];
     const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
     if (!load_tile_blocks(a, mt, tb)) return;
     Epilogue<BF16, BM, BN> epi;
-    epi.prefetch(a, tb, n0, s_bias);
+    epi.prefetch(a, tb, n0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int kwc = KS * a.cin;            // values per kernel row, <= 32
@@ -712,7 +764,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
 #pragma unroll
             for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
     }
-    epi.finish(a, acc, smem, n0, s_bias);
+    epi.finish(a, acc, smem, n0);
 }
 
 // ------------------------------------------------------------------ planning
@@ -804,13 +856,34 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
     return true;
 }
 
-// Tiles: the largest that still give a full frame >= 2048 workgroups (about 600 at
-// 30 % of the blocks active), else the most workgroups. Pipelined layers that still
-// have fewer than 2048 tiles split K (at least 2 chunks per slice, at most 8 slices).
-// The choice depends on the layer's shape only, never on the active count, so an
-// active block's result does not depend on which other blocks are active.
+// Tile choice for the pipelined form (1x1 and 3x3 layers), from a sweep of tile shape
+// and K split over every ResNet-50 layer of a 2048x1024 frame with 30 % of the blocks
+// active: 64-row tiles are fastest everywhere (at these sizes the kernel is bound by
+// latency and occupancy, and 64x64 tiles keep the most workgroups resident); 128-wide N
+// tiles pay off only for 1x1 layers with 64 input channels; splitting K pays off only
+// when a full frame has at most 256 tiles (the stride-32 layers), and then by 2.
+// Other forms take the largest tile with >= 2048 workgroups on a full frame. The choice
+// depends on the layer's shape only, never on the active count, so an active block's
+// result does not depend on which other blocks are active.
 bool choose_plan(const LayerGeom &g, Plan &best)
 {
+    if ((g.kh == 1 || g.kh == 3) && g.cin % 8 == 0) {
+        const int bn = (g.kh == 1 && g.cin <= 64 && g.cout >= 256 && g.cout % 128 == 0) ? 128 : 64;
+        if (make_plan(g, 64, bn, best) || make_plan(g, 64, 64, best)) {
+            MfmaArgs &a = best.a;
+            const int nchunk = (g.cin + BK - 1) / BK;
+            const unsigned tiles = best.grid;
+            if (best.BM == 64 && best.BN == 64 && tiles <= 256 && nchunk >= 8 &&
+                tiles <= (unsigned)kMaxSplitTiles) {
+                a.cps = (nchunk + 1) / 2;
+                a.ksplit = (nchunk + a.cps - 1) / a.cps;
+                best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
+                best.grid = tiles * a.ksplit;
+            }
+            best.a.tiles_full = (int)best.grid;
+            return true;
+        }
+    }
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
     bool have = false;
     for (const auto &c : cand) {
@@ -823,26 +896,8 @@ bool choose_plan(const LayerGeom &g, Plan &best)
             break;
         }
     }
-    if (!have) return false;
-    if (best.form == Form::Pipe) {
-        MfmaArgs &a = best.a;
-        const int nchunk = (g.cin + BK - 1) / BK;
-        const unsigned tiles = best.grid;
-        int ks = 1;
-        while (ks < 8 && tiles * ks < 2048 && nchunk >= 4 * ks) ks *= 2;
-        a.cps = (nchunk + ks - 1) / ks;
-        a.ksplit = (nchunk + a.cps - 1) / a.cps;
-        if (a.ksplit > 1) {
-            if (tiles > (unsigned)kMaxSplitTiles) {
-                a.ksplit = 1;
-                a.cps = nchunk;
-            } else {
-                best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
-            }
-        }
-        best.grid = tiles * a.ksplit;
-    }
-    return true;
+    if (have) best.a.tiles_full = (int)best.grid;
+    return have;
 }
 
 // Split-K workspace: one per device, grown on demand (never during a call that is
@@ -976,6 +1031,10 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     a.x_bytes = (int)((size_t)g.n * g.hin * g.win * g.cin * 2);
     a.w_bytes = (int)((size_t)g.cout * g.kh * g.kw * g.cin * 2);
     a.y_bytes = (int)((size_t)g.n * g.hout * g.wout * g.cout * 2);
+    a.f_hrhc = make_fastdiv(a.HR * a.HC > 0 ? a.HR * a.HC : 1);
+    a.f_hc = make_fastdiv(a.HC > 0 ? a.HC : 1);
+    a.f_rbw = make_fastdiv(a.R * g.bw);
+    a.f_bw = make_fastdiv(g.bw);
     if (p.grid == 0) return hipSuccess;
     if (p.ws_bytes) {
         hipError_t e = workspace(p.ws_bytes, &a.ws);
