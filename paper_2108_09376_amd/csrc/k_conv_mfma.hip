@@ -682,63 +682,110 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 }
 
 // ------------------------------------------------------------------ stem form
+//
+// Layers with few input channels (the RGB stem): Cin <= 4 with kw <= 8, or Cin <= 8 with
+// kw <= 4. In LDS every input pixel carries CP = 4 (or 8) channels, zero-padded, so one
+// kernel row of one output pixel is a run of kw*CP <= 32 values and one MFMA k step
+// covers it: k = j*CP + c for tap column j and channel c (k with j >= kw or c >= Cin
+// meets zero weights). A lane's 8 consecutive k are then 16 contiguous bytes of LDS.
+// Weights arrive as one contiguous [BN][kh*kw*Cin] run (16-byte buffer loads) and are
+// rearranged in LDS into the padded [kh][BN][32] k order.
 
-template <bool BF16, int BM, int BN, int KS, int S>
+template <bool BF16, int BM, int BN, int KS, int S, int CP>
 __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
 {
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int MI = WM / 16, NI = WN / 16;
-    constexpr int BKP = 40;  // elements per LDS weight row (32 + 8 pad)
+    constexpr int BKP = 40;                  // elements per LDS weight row (32 + 8 pad)
+    constexpr int PPK = 8 / CP;              // pixels per 8 consecutive k
+    static_assert(BN == 64, "stem form: one 64-channel N tile per workgroup");
     extern __shared__ __align__(16) uint8_t smem[];
 
     __shared__ TileBlocks tb;
     const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
     if (!load_tile_blocks(a, mt, tb)) return;
-    Epilogue<BF16, BM, BN> epi;
-    epi.prefetch(a, tb, n0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int kwc = KS * a.cin;            // values per kernel row, <= 32
-    const int rp = a.rowpitch;             // elements per halo row (>= HC*cin + 32)
-    uint16_t *sA = (uint16_t *)smem;                       // [P][HR][rp]
-    uint16_t *sB = sA + (size_t)a.P * a.HR * rp;           // [KS][BN][BKP]
+    const int hcp = a.rowpitch;              // pixels per LDS halo row (>= (bw-1)*S + 32/CP)
+    const int kwc = KS * a.cin;              // weight values per kernel row
+    const int wvals = BN * KS * kwc;         // weights of this N tile
+    uint8_t *sA = smem;                                              // [P][HR][hcp][CP]
+    const int a_bytes = ((a.P * a.HR * hcp * CP * 2) + 15) & ~15;
+    uint16_t *sB = (uint16_t *)(smem + a_bytes);                     // [KS][BN][BKP]
+    uint16_t *sW = sB + KS * BN * BKP;                               // raw [BN][KS*kwc]
 
-    // stage halo rows: raw channels-last runs, zero outside the image and in the tail
-    const int rowvals = a.HC * a.cin;
-    const int nrows = a.P * a.HR;
-    for (int e = tid; e < nrows * rp; e += kThreads) {
-        const int row = e / rp, t = e - (e / rp) * rp;
-        const int p = row / a.HR, ra = row - (row / a.HR) * a.HR;
-        uint16_t v = 0;
+    // raw weights of the N tile: one contiguous run, 16-byte requests
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
+    const int wbase = n0 * KS * kwc * 2;
+    const int nvec = (wvals * 2 + 15) / 16;
+    for (int v = tid; v < nvec; v += kThreads)
+        *(uint4 *)((uint8_t *)sW + v * 16) = bload(wr, wbase + v * 16);
+    Epilogue<BF16, BM, BN> epi;
+    epi.prefetch(a, tb, n0);
+
+    // halo pixels with CP channels each (zeros outside the image, past Cin, in the tail)
+    const int npix = a.P * a.HR * hcp;
+    for (int e = tid; e < npix; e += kThreads) {
+        const int row = fdiv(e, a.f_hc);                  // f_hc holds 1 / hcp here
+        const int col = e - row * hcp;
+        const int p = fdiv(row, a.f_hrhc);               // f_hrhc holds 1 / HR here
+        const int hy = row - p * a.HR;
+        uint16_t v[CP];
+#pragma unroll
+        for (int c = 0; c < CP; ++c) v[c] = 0;
         const int img = tb.img[p];
-        if (t < rowvals && img >= 0) {
-            const int rb = t / a.cin, ch = t - (t / a.cin) * a.cin;
-            const int iy = tb.oy0[p] * S - a.pad + ra, ix = tb.ox0[p] * S - a.pad + rb;
-            if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
-                v = a.x[(((size_t)img * a.hin + iy) * a.win + ix) * a.cin + ch];
+        const int iy = tb.oy0[p] * S - a.pad + hy, ix = tb.ox0[p] * S - a.pad + col;
+        if (img >= 0 && col < a.HC && iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win) {
+            const uint16_t *src = a.x + (((size_t)img * a.hin + iy) * a.win + ix) * a.cin;
+#pragma unroll
+            for (int c = 0; c < CP; ++c)
+                if (c < a.cin) v[c] = src[c];
         }
-        sA[e] = v;
+        if constexpr (CP == 4) {
+            *(uint2 *)(sA + (size_t)e * 8) = make_uint2(v[0] | ((uint32_t)v[1] << 16),
+                                                        v[2] | ((uint32_t)v[3] << 16));
+        } else {
+            *(uint4 *)(sA + (size_t)e * 16) = make_uint4(
+                v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+        }
     }
-    // stage weights: B[i][n][kk] = W[n0 + n][i][kk] for kk < kw*cin, else 0
-    for (int e = tid; e < KS * BN * BKP; e += kThreads) {
-        const int i = e / (BN * BKP);
-        const int r = e - i * BN * BKP;
-        const int n = r / BKP, kk = r - (r / BKP) * BKP;
-        sB[e] = kk < kwc ? a.w[((size_t)(n0 + n) * KS + i) * kwc + kk] : (uint16_t)0;
+    __syncthreads();
+    // rearrange weights: B[i][n][kk] = W[n][i][j][c] with kk = j*CP + c, zero elsewhere
+    {
+        const int n = tid >> 2, kq = tid & 3;
+        const uint16_t *src = sW + n * KS * kwc;
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+            uint32_t w2[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                uint32_t pr = 0;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int kk = kq * 8 + t * 2 + h;
+                    const int j = kk / CP, c = kk % CP;
+                    const uint32_t val = (j < KS && c < a.cin) ? src[i * kwc + j * a.cin + c] : 0u;
+                    pr |= val << (16 * h);
+                }
+                w2[t] = pr;
+            }
+            *(uint4 *)(sB + (i * BN + n) * BKP + kq * 8) = make_uint4(w2[0], w2[1], w2[2], w2[3]);
+        }
     }
     __syncthreads();
 
     const int rbw = a.R * a.bw;
-    int arow[MI], acol[MI];
+    int aoffs[MI];
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
         const int m = wm * WM + mi * 16 + (lane & 15);
-        const int p = m / rbw;
+        const int p = fdiv(m, a.f_rbw);
         const int local = m - p * rbw;
-        const int pr = local / a.bw, pc = local - (local / a.bw) * a.bw;
-        arow[mi] = (p * a.HR + pr * S) * rp;
-        acol[mi] = pc * S * a.cin + (lane >> 4) * 8;
+        const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
+        aoffs[mi] = ((p * a.HR + pr * S) * hcp + pc * S + (lane >> 4) * PPK) * CP * 2;
     }
     f32x4 acc[MI][NI];
 #pragma unroll
@@ -746,18 +793,22 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+#pragma unroll
     for (int i = 0; i < KS; ++i) {
         short8 af[MI], bf[NI];
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi) {
-            const uint16_t *src = sA + arow[mi] + i * rp + acol[mi];
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                af[mi][j] = ((lane >> 4) * 8 + j < kwc) ? (short)src[j] : (short)0;
+            const uint8_t *src = sA + aoffs[mi] + i * hcp * CP * 2;
+            if constexpr (CP == 8 || S % 2 == 0) {
+                af[mi] = *(const short8 *)src;                  // 16-byte aligned
+            } else {
+                const uint2 lo = *(const uint2 *)src, hi = *(const uint2 *)(src + 8);
+                af[mi] = __builtin_bit_cast(short8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+            }
         }
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-            bf[ni] = *(const short8 *)(sB + ((size_t)i * BN + wn * WN + ni * 16 + (lane & 15)) * BKP +
+            bf[ni] = *(const short8 *)(sB + (i * BN + wn * WN + ni * 16 + (lane & 15)) * BKP +
                                        (lane >> 4) * 8);
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
@@ -816,14 +867,17 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
     pl.ws_bytes = 0;
     if (g.cin % 8) {
         pl.form = Form::Stem;
-        if (KS * g.cin > 32 || BN != 64) return false;
+        const int CP = g.cin <= 4 ? 4 : 8;
+        if (g.cin > 8 || KS * CP > 32 || BN != 64) return false;
         a.HR = (a.R - 1) * S + KS;
         a.HC = (g.bw - 1) * S + KS;
-        a.rowpitch = ((a.HC * g.cin + 32) + 7) / 8 * 8;
+        a.rowpitch = (((g.bw - 1) * S + 32 / CP) + 1) & ~1;   // pixels per LDS halo row, even
         a.nslot = 0;
-        const size_t main = (size_t)a.P * a.HR * a.rowpitch * 2 + (size_t)KS * BN * 40 * 2;
+        const size_t abytes = ((size_t)a.P * a.HR * a.rowpitch * CP * 2 + 15) & ~(size_t)15;
+        const size_t main = abytes + (size_t)KS * BN * 40 * 2 +
+                            (((size_t)BN * KS * KS * g.cin * 2 + 15) & ~(size_t)15);
         pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
-        if (pl.lds > kMaxLds) return false;
+        if (pl.lds > kMaxLdsPipe) return false;
     } else {
         if (KS == 1) {
             a.HR = a.R;
@@ -952,7 +1006,10 @@ template <bool BF16, int BM, int BN, int KS, int S>
 void launch_one(const Plan &p, hipStream_t s)
 {
     if (p.form == Form::Stem) {
-        launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S>, p, s);
+        if constexpr (BN == 64) {
+            if (p.a.cin <= 4) launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 4>, p, s);
+            else if constexpr (KS <= 4) launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 8>, p, s);
+        }
     } else if (p.form == Form::Pipe) {
         if constexpr (KS == 1 || KS == 3) launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, kPipeStages>, p, s);
     } else {
@@ -994,8 +1051,9 @@ bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why)
         *why = "matrix-core path: Cout must be a multiple of 64";
         return false;
     }
-    if (g.cin % 8 && g.kw * g.cin > 32) {
-        *why = "matrix-core path: Cin must be a multiple of 8, or kw*Cin <= 32 (stem form)";
+    if (g.cin % 8 && !(g.cin <= 4 && g.kw <= 7) && !(g.cin < 8 && g.kw <= 3)) {
+        *why = "matrix-core path: Cin must be a multiple of 8, or Cin <= 4 with a kernel edge "
+               "<= 7, or Cin < 8 with a kernel edge <= 3 (stem form)";
         return false;
     }
     if (2.0 * g.n * g.hin * g.win * g.cin >= 2147483392.0 ||
@@ -1031,8 +1089,13 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     a.x_bytes = (int)((size_t)g.n * g.hin * g.win * g.cin * 2);
     a.w_bytes = (int)((size_t)g.cout * g.kh * g.kw * g.cin * 2);
     a.y_bytes = (int)((size_t)g.n * g.hout * g.wout * g.cout * 2);
-    a.f_hrhc = make_fastdiv(a.HR * a.HC > 0 ? a.HR * a.HC : 1);
-    a.f_hc = make_fastdiv(a.HC > 0 ? a.HC : 1);
+    if (p.form == Form::Stem) {            // stem form: divisions by the halo row pitch and HR
+        a.f_hc = make_fastdiv(a.rowpitch);
+        a.f_hrhc = make_fastdiv(a.HR);
+    } else {
+        a.f_hrhc = make_fastdiv(a.HR * a.HC > 0 ? a.HR * a.HC : 1);
+        a.f_hc = make_fastdiv(a.HC > 0 ? a.HC : 1);
+    }
     a.f_rbw = make_fastdiv(a.R * g.bw);
     a.f_bw = make_fastdiv(g.bw);
     if (p.grid == 0) return hipSuccess;
