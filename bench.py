@@ -41,6 +41,13 @@ def parse():
     ap.add_argument("--sweep", default="0.1,0.5,1.0", help="extra active fractions timed (comma list, '' for none)")
     ap.add_argument("--no-graph", action="store_true", help="launch layer by layer instead of a HIP graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gather-scatter", action="store_true")
+    ap.add_argument("--no-clip", action="store_true", help="skip the ResNet-18 30-frame clip")
+    ap.add_argument("--pmc-frames", type=int, default=0,
+                    help="rocprofv3 --pmc helper: a 256 MiB copy (calibration) then N sparse frames "
+                         "at --frac launched layer by layer; prints nothing else")
+    ap.add_argument("--no-layer-sweep", action="store_true",
+                    help="skip the single-layer shapes (256x512x64 3x3; stride-16 C sweep)")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only N plain steps (for rocprofv3) and print nothing else")
     ap.add_argument("--rocprof-summary", metavar="KERNEL_STATS_CSV",
@@ -76,6 +83,178 @@ def cpu_baseline(mask):
             "kind": "oracle",
             "sample": "ResNet-50 layer1.0 (4 convs) at 256x512x64 bf16, dense-then-select in fp64, "
                       f"{int((mask != 0).sum())}/{gh * gw} blocks active; {dt:.1f} s"}
+
+
+def layer_sweep(torch, bc, dev):
+    """Single block-sparse layers at their 2048x1024-frame shapes, 38 of 128 blocks
+    active (clustered): the stride-4 3x3 64->64 layer (256x512, 32-px blocks) and the
+    stride-16 sweep (64x128, 8-px blocks), 1x1 and 3x3 with Cin = Cout in {256, 512,
+    1024}. Each is timed as a captured graph of 10 launches; FLOPs are algorithmic
+    (2*Cin*Cout*k*k per active output pixel)."""
+    import numpy as np
+
+    import synth
+    shapes = [("3x3 64->64 @256x512", 64, 64, 256, 512, 3)]
+    for c in (256, 512, 1024):
+        for k in (1, 3):
+            shapes.append((f"{k}x{k} {c}->{c} @64x128", c, c, 64, 128, k))
+    mask = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
+    m = torch.from_numpy(mask).to(dev)
+    idx = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
+    out = {}
+    r = synth.rng(synth.SEED_WEIGHT0)
+    for name, cin, cout, h, w, k in shapes:
+        x = torch.from_numpy(synth.to_storage_bits(synth.normal(r, (1, h, w, cin)), "bf16").view(np.int16)).view(torch.bfloat16).to(dev)
+        wt = torch.from_numpy(bc.bc_repack_weights(synth.he_normal(r, cout, cin, k, k), bc.BC_BF16).view(np.int16)).view(torch.bfloat16).to(dev)
+        b = torch.zeros(cout, dtype=torch.float32, device=dev)
+        y = torch.zeros((1, h, w, cout), dtype=torch.bfloat16, device=dev)
+        call = lambda: bc.bc_sparse_conv2d((k, k, 1, k // 2, 1), x, bc.BC_NHWC, wt, b, None, y, (8, 16), idx, cnt)
+        call()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                call()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / 50
+        fl = 2.0 * cin * cout * k * k * h * w * int(mask.sum()) / mask.size
+        out[name] = {"us": round(us, 2), "tflops": round(fl / us / 1e6, 1),
+                     "frac_of_mfma_peak": round(fl / us / 1e6 / PEAK_BF16_TFLOPS, 4)}
+        del g
+    return out
+
+
+def gather_scatter(torch, bc, dev):
+    """Standalone halo gather and block scatter on the 256x512 stride-4 map of a
+    2048x1024 frame (32-px blocks, 38 of 128 active, 3x3 halo), C = 64 and 256, bf16.
+    Algorithmic bytes: gather reads and writes every halo tile element once, scatter
+    reads and writes every block element once. 'warm': graph of 10 launches (inputs
+    can stay in the 256 MB last-level cache); 'cold': each launch follows a 512 MiB
+    write that evicts the caches (graph-differenced, see below)."""
+    import numpy as np
+
+    import synth
+    mask = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
+    n_act = int(mask.sum())
+    m = torch.from_numpy(mask).to(dev)
+    idx = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    out = {}
+    for c in (64, 256):
+        x = torch.randn((1, 256, 512, c), device=dev).to(torch.bfloat16)
+        packed = torch.empty((128, 34, 34, c), dtype=torch.bfloat16, device=dev)
+        blocks = torch.randn((128, 32, 32, c), device=dev).to(torch.bfloat16)
+        dst = torch.empty_like(x)
+        ops = {
+            "gather": (lambda: bc.bc_gather_halo(x, bc.BC_NHWC, (8, 16), (3, 3, 1, 1, 0), 0.0, idx, cnt, packed),
+                       2 * n_act * 34 * 34 * c * 2),
+            "scatter": (lambda: bc.bc_scatter_blocks(blocks, idx, cnt, (8, 16), dst, bc.BC_NHWC),
+                        2 * n_act * 32 * 32 * c * 2),
+        }
+        for name, (fn, nbytes) in ops.items():
+            fn()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(10):
+                    fn()
+            g.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(5):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            warm = e0.elapsed_time(e1) * 1e3 / 50
+            # Cold: a graph of 5 x (512 MiB cache-evicting fill, op) minus a graph of the
+            # 5 fills alone, so launch latency is amortised as in a captured frame.
+            def timed(with_op):
+                gg = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gg):
+                    for _ in range(5):
+                        flush.fill_(1)
+                        if with_op:
+                            fn()
+                gg.replay()
+                torch.cuda.synchronize()
+                ts = []
+                for _ in range(3):
+                    e0.record()
+                    gg.replay()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    ts.append(e0.elapsed_time(e1) * 1e3 / 5)
+                del gg
+                return float(np.median(ts))
+            cold_us = timed(True) - timed(False)
+            out[f"{name}_C{c}"] = {"bytes": nbytes, "warm_us": round(warm, 2),
+                                   "warm_GBps": round(nbytes / warm / 1e3, 1),
+                                   "cold_us": round(cold_us, 2),
+                                   "cold_GBps": round(nbytes / cold_us / 1e3, 1),
+                                   "cold_frac_of_hbm_peak": round(nbytes / cold_us / 1e3 / PEAK_HBM_GBS, 3)}
+            del g
+    return out
+
+
+def resnet18_clip(torch, dev, frames=30):
+    """ResNet-18 encoder (random init, bf16) on a 30-frame synthetic 2048x1024 clip:
+    moving textured rectangles over a smooth background, execution grid = blocks
+    touched by an object at t or t-1, frame 0 on every block. Frame 0 runs eagerly;
+    every later frame replays one captured sparse-frame graph (block index built inside
+    it) after the frame's image and grid are copied into the graph's fixed device
+    buffers. Returns mean ms over frames 1..29 and the mean active fraction."""
+    import numpy as np
+
+    import synth
+    from paper_2108_09376_amd import resnet
+    clip = synth.SyntheticClip(synth.SEED_INPUT + 4)
+    net = resnet.SparseResNet(18, 1024, 2048, 128, device=dev)
+    x = torch.empty((1, 1024, 2048, 3), dtype=torch.bfloat16, device=dev)
+
+    def load(t):
+        img = synth.to_storage_bits(clip.frame(t), "bf16")
+        x.copy_(torch.from_numpy(img.view(np.int16)).view(torch.bfloat16))
+        mask = clip.mask(t)
+        net.set_mask(mask)
+        torch.cuda.synchronize()
+        return mask
+
+    load(0)
+    net.frame(x, sparse=False)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        net.frame(x, sparse=True)
+    times, fracs = [], []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    load(0)
+    net.frame(x, sparse=False)           # the capture did not run; restart the clip
+    for t in range(1, frames):
+        mask = load(t)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+        fracs.append(float(mask.mean()))
+    flops = sum(net.conv_flops(int(round(f * 128))) for f in fracs) / len(fracs)
+    ms = float(np.mean(times))
+    return {"frames": frames, "mean_ms_per_sparse_frame": round(ms, 4),
+            "mean_active_fraction": round(float(np.mean(fracs)), 4),
+            "effective_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 2),
+            "launch": "one HIP graph replay per sparse frame"}
 
 
 def rocprof_summary(path):
@@ -128,6 +307,19 @@ def main():
 
     net.frame(x, sparse=False)           # frame 0 of the clip: every block
     torch.cuda.synchronize()
+
+    if args.pmc_frames:
+        a0 = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        a1 = torch.empty_like(a0)
+        a0.fill_(1)
+        torch.cuda.synchronize()
+        a1.copy_(a0)                      # calibration: 256 MiB read + 256 MiB written
+        torch.cuda.synchronize()
+        net.set_mask(masks_for(args.frac))
+        for _ in range(args.pmc_frames):
+            net.frame(x, sparse=True)
+        torch.cuda.synchronize()
+        return
 
     if args.profile_steps:
         net.set_mask(masks_for(args.frac))
@@ -236,6 +428,12 @@ def main():
                      "traffic": None,
                      "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
+    if not args.no_layer_sweep:
+        out["single_layers_at_0.3"] = layer_sweep(torch, bc, dev)
+    if not args.no_gather_scatter:
+        out["gather_scatter"] = gather_scatter(torch, bc, dev)
+    if not args.no_clip:
+        out["resnet18_clip"] = resnet18_clip(torch, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mask)
     print(json.dumps(out))

@@ -3,9 +3,9 @@
 //
 // Both are pure HBM streams. With channels-last storage a tile row of the halo is
 // one contiguous run of tw*C elements in the source and in the packed tile, and a
-// block row of the destination is one contiguous run of bw*C elements, so one
-// workgroup copies one row with 16-byte vector accesses whenever C*esize is a
-// multiple of 16. Channels-first sources are transposed element by element (the
+// block row of the destination is one contiguous run of bw*C elements, so whenever
+// C*esize is a multiple of 16 the copies use 16-byte vectors, a fixed-size chunk of a
+// tile per workgroup. Channels-first sources are transposed element by element (the
 // fp32 correctness path). Workgroups beyond the device-side active count exit at
 // once; destination elements outside active blocks are never touched.
 #include "bc_internal.h"
@@ -39,6 +39,96 @@ __device__ __forceinline__ void block_origin(const int32_t *idx, int k, const Ro
 
 // ---------------------------------------------------------------- channels last
 
+// Channels last, 16-byte vectors: a packed tile is th*tw*vpp contiguous vectors, and a
+// workgroup copies one chunk of kVecPerWG of them; each thread issues all of its loads
+// before any store, so the whole chunk is in flight at once.
+constexpr int kVecPerThread = 4;
+constexpr int kVecPerWG = kThreads * kVecPerThread;
+
+__global__ __launch_bounds__(kThreads) void k_gather_nhwc16(const uint4 *__restrict__ src,
+                                                            uint4 *__restrict__ packed, RowGeom g,
+                                                            int vpp, int chunks, uint4 padv,
+                                                            const int32_t *__restrict__ idx,
+                                                            const int32_t *__restrict__ count)
+{
+    const int k = blockIdx.x / chunks;
+    const int chunk = blockIdx.x - k * chunks;
+    if (k >= active_count(count, g.total_blocks)) return;
+    int img, gy, gx;
+    block_origin(idx, k, g, img, gy, gx);
+    const int rowv = g.tw * vpp;
+    const int nv = g.th * rowv;
+    const int x0 = gx * g.bw * g.stride - g.pad;
+    const int y0 = gy * g.bh * g.stride - g.pad;
+    uint4 *out = packed + (size_t)k * nv;
+    // Every load reads a valid address (indices clamped into the image) and the padding
+    // is selected afterwards: no load sits under a branch, so all of them are in flight
+    // together instead of each waiting for the previous one.
+    uint4 val[kVecPerThread];
+    bool in_img[kVecPerThread];
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u) {
+        const int v = min(chunk * kVecPerWG + u * kThreads + (int)threadIdx.x, nv - 1);
+        const int r = v / rowv;
+        const int t = v - r * rowv;
+        const int tx = t / vpp;
+        const int iy = y0 + r, ix = x0 + tx;
+        in_img[u] = iy >= 0 && iy < g.h && ix >= 0 && ix < g.w;
+        const int cy = min(max(iy, 0), g.h - 1), cx = min(max(ix, 0), g.w - 1);
+        val[u] = src[(((size_t)img * g.h + cy) * g.w + cx) * vpp + (t - tx * vpp)];
+    }
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u)
+        if (!in_img[u]) val[u] = padv;
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u) {
+        const int v = chunk * kVecPerWG + u * kThreads + threadIdx.x;
+        if (v < nv) out[v] = val[u];
+    }
+}
+
+// Raw buffer resource (no swizzle, dword format): stores at byte offsets at or beyond
+// num_records are dropped, which lets the ragged end of a chunk store unconditionally.
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kOutOfRange = 0x7FFFFF00;
+
+__global__ __launch_bounds__(kThreads) void k_scatter_nhwc16(const uint4 *__restrict__ packed,
+                                                             uint4 *__restrict__ dst, RowGeom g,
+                                                             int vpp, int chunks,
+                                                             const int32_t *__restrict__ idx,
+                                                             const int32_t *__restrict__ count)
+{
+    const int k = blockIdx.x / chunks;
+    const int chunk = blockIdx.x - k * chunks;
+    if (k >= active_count(count, g.total_blocks)) return;
+    int img, gy, gx;
+    block_origin(idx, k, g, img, gy, gx);
+    const int rowv = g.bw * vpp;
+    const int nv = g.bh * rowv;
+    const int pitch = g.w * vpp;                 // vectors per destination image row
+    const uint4 *in = packed + (size_t)k * nv;
+    uint4 *out = dst + (((size_t)img * g.h + (size_t)gy * g.bh) * g.w + (size_t)gx * g.bw) * vpp;
+    // The block's footprint in dst: bh rows of rowv vectors, pitch apart (below 2 GiB,
+    // checked by the launcher).
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)out, (short)0, ((g.bh - 1) * pitch + rowv) * 16, kBufferFlags);
+    uint4 val[kVecPerThread];
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u)     // clamped: unconditional loads, all in flight
+        val[u] = in[min(chunk * kVecPerWG + u * kThreads + (int)threadIdx.x, nv - 1)];
+#pragma unroll
+    for (int u = 0; u < kVecPerThread; ++u) {
+        const int v = chunk * kVecPerWG + u * kThreads + threadIdx.x;
+        const int row = v / rowv;
+        const int off = v < nv ? (row * pitch + (v - row * rowv)) * 16 : kOutOfRange;
+        const uint4 x = val[u];
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(__attribute__((ext_vector_type(4))) int, x), r, off, 0, 0);
+    }
+}
+
+// Element-wise channels-last fallback (C * esize not a multiple of 16): one tile row per
+// workgroup.
 template <typename V>
 __global__ __launch_bounds__(kThreads) void k_gather_nhwc(const V *__restrict__ src,
                                                           V *__restrict__ packed, RowGeom g,
@@ -163,8 +253,11 @@ hipError_t launch_gather_halo(const void *src, int esize, bool nhwc, const Layer
     if (nhwc && (g.c * esize) % 16 == 0) {
         const uint32_t p = esize == 2 ? (pad_bits & 0xFFFFu) * 0x10001u : pad_bits;
         const uint4 padv = make_uint4(p, p, p, p);
-        hipLaunchKernelGGL(k_gather_nhwc<uint4>, grid, block, 0, s, (const uint4 *)src,
-                           (uint4 *)packed, g, g.c * esize / 16, padv, L.idx, L.count);
+        const int vpp = g.c * esize / 16;
+        const int chunks = (g.th * g.tw * vpp + kVecPerWG - 1) / kVecPerWG;
+        hipLaunchKernelGGL(k_gather_nhwc16, dim3((unsigned)L.total_blocks * chunks), block, 0, s,
+                           (const uint4 *)src, (uint4 *)packed, g, vpp, chunks, padv, L.idx,
+                           L.count);
     } else if (nhwc && esize == 2) {
         hipLaunchKernelGGL(k_gather_nhwc<uint16_t>, grid, block, 0, s, (const uint16_t *)src,
                            (uint16_t *)packed, g, g.c, (uint16_t)pad_bits, L.idx, L.count);
@@ -186,9 +279,12 @@ hipError_t launch_scatter_blocks(const void *packed, int esize, bool nhwc, const
 {
     const RowGeom g = row_geom(L, false);
     const dim3 grid((unsigned)L.total_blocks * g.bh), block(kThreads);
-    if (nhwc && (g.c * esize) % 16 == 0) {
-        hipLaunchKernelGGL(k_scatter_nhwc<uint4>, grid, block, 0, s, (const uint4 *)packed,
-                           (uint4 *)dst, g, g.c * esize / 16, L.idx, L.count);
+    const int64_t span = nhwc ? ((int64_t)(g.bh - 1) * g.w + g.bw) * g.c * esize : 0;
+    if (nhwc && (g.c * esize) % 16 == 0 && span < kOutOfRange) {
+        const int vpp = g.c * esize / 16;
+        const int chunks = (g.bh * g.bw * vpp + kVecPerWG - 1) / kVecPerWG;
+        hipLaunchKernelGGL(k_scatter_nhwc16, dim3((unsigned)L.total_blocks * chunks), block, 0, s,
+                           (const uint4 *)packed, (uint4 *)dst, g, vpp, chunks, L.idx, L.count);
     } else if (nhwc && esize == 2) {
         hipLaunchKernelGGL(k_scatter_nhwc<uint16_t>, grid, block, 0, s, (const uint16_t *)packed,
                            (uint16_t *)dst, g, g.c, L.idx, L.count);

@@ -47,7 +47,8 @@ def test_block_index_bit_exact(B, n, gh, gw, p):
 # ------------------------------------------------------------------ a2 / a5: gather, scatter
 
 @pytest.mark.parametrize("dtype,nhwc,c", [("bf16", True, 64), ("bf16", True, 12), ("f16", True, 24),
-                                          ("f32", True, 8), ("f32", False, 16), ("f32", False, 3)])
+                                          ("f32", True, 8), ("f32", False, 16), ("f32", False, 3),
+                                          ("bf16", True, 520)])
 @pytest.mark.parametrize("k,s,p", [(3, 1, 1), (1, 1, 0), (3, 2, 1), (7, 2, 3)])
 def test_gather_halo_bit_exact(B, dtype, nhwc, c, k, s, p):
     r = synth.rng(50 + c + k)
@@ -73,7 +74,8 @@ def test_gather_halo_bit_exact(B, dtype, nhwc, c, k, s, p):
     assert not got[cnt_np:].any() and not sent.any()
 
 
-@pytest.mark.parametrize("dtype,nhwc,c", [("bf16", True, 64), ("bf16", True, 12), ("f32", False, 16)])
+@pytest.mark.parametrize("dtype,nhwc,c", [("bf16", True, 64), ("bf16", True, 12), ("f32", False, 16),
+                                          ("bf16", True, 520)])
 def test_scatter_blocks_bit_exact_and_untouched(B, dtype, nhwc, c):
     r = synth.rng(60 + c)
     h, w, gh, gw = 32, 48, 4, 3
