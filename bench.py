@@ -44,45 +44,59 @@ def parse():
     ap.add_argument("--no-gather-scatter", action="store_true")
     ap.add_argument("--no-clip", action="store_true", help="skip the ResNet-18 30-frame clip")
     ap.add_argument("--pmc-frames", type=int, default=0,
-                    help="rocprofv3 --pmc helper: a 256 MiB copy (calibration) then N sparse frames "
+                    help="rocprofv3 --pmc helper: a 256 MiB float32 negation (calibration) then N sparse frames "
                          "at --frac launched layer by layer; prints nothing else")
     ap.add_argument("--no-layer-sweep", action="store_true",
                     help="skip the single-layer shapes (256x512x64 3x3; stride-16 C sweep)")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only N plain steps (for rocprofv3) and print nothing else")
-    ap.add_argument("--rocprof-summary", metavar="KERNEL_STATS_CSV",
-                    help="print a text summary of a rocprofv3 --stats kernel table and exit")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the HBM-traffic summary of two counter_collection.csv files and exit")
+    ap.add_argument("--rocprof-summary", nargs="+", metavar="CSV",
+                    help="KERNEL_STATS_CSV [KERNEL_TRACE_CSV FIRST COUNT]: print a text summary of a "
+                         "rocprofv3 --stats kernel table (and a window of conv dispatches) and exit")
     return ap.parse_args()
 
 
 def cpu_baseline(mask):
     """The CPU oracle (dense convolution then masked select, fp64, OpenMP) on a bounded
-    sample of the workload: the four convolutions of ResNet-50 layer1.0 (1x1 64->64,
-    3x3 64->64, 1x1 64->256, 1x1 64->256 shortcut) at their real 256x512 size with
-    the frame's mask. Rate = active-block FLOPs of the sample / oracle time."""
+    sample of the workload: every convolution of ResNet-50's first two stages (layer1
+    and layer2: 23 convs, stride 4 and 8) at their real sizes for a 2048x1024 frame, with
+    the frame's mask; each layer gets seeded bf16 inputs of its shape. Rate = the
+    sample's active-block FLOPs / oracle time."""
     import numpy as np
 
     import oracle
     import synth
+    from paper_2108_09376_amd import resnet
+    layers = resnet.build_layers(50)
+    shapes = resnet.layer_shapes(layers, 1024, 2048)
     r = synth.rng(5)
-    h, w = 256, 512
-    layers = [(64, 64, 1, False), (64, 64, 3, False), (64, 256, 1, True), (64, 256, 1, False)]
-    x = synth.to_storage_bits(synth.normal(r, (1, 64, h, w)), "bf16")
     gh, gw = mask.shape[1:]
     act = int((mask != 0).sum()) / (gh * gw)
     flops = 0.0
-    t0 = time.perf_counter()
-    for cin, cout, k, res in layers:
-        wt = synth.to_storage_bits(synth.he_normal(r, cout, cin, k, k), "bf16")
-        prev = np.zeros((1, cout, h, w), np.uint16)
-        rb = synth.to_storage_bits(synth.normal(r, (1, cout, h, w)), "bf16") if res else None
-        oracle.sparse_conv2d(x, wt, mask, prev, "bf16", 1, k // 2, np.zeros(cout, np.float32), rb, True)
-        flops += 2.0 * cin * cout * k * k * h * w * act
-    dt = time.perf_counter() - t0
+    n = 0
+    dt = 0.0
+    for i, l in enumerate(layers):
+        if l.kind != "conv" or not l.name.startswith(("layer1", "layer2")):
+            continue
+        ih, iw = shapes[l.src][:2]
+        oh, ow = shapes[i][:2]
+        x = synth.to_storage_bits(synth.normal(r, (1, l.cin, ih, iw)), "bf16")
+        wt = synth.to_storage_bits(synth.he_normal(r, l.cout, l.cin, l.k, l.k), "bf16")
+        prev = np.zeros((1, l.cout, oh, ow), np.uint16)
+        rb = synth.to_storage_bits(synth.normal(r, (1, l.cout, oh, ow)), "bf16") if l.res is not None else None
+        t0 = time.perf_counter()           # the oracle only, not the input generation
+        oracle.sparse_conv2d(x, wt, mask, prev, "bf16", l.stride, l.pad, np.zeros(l.cout, np.float32), rb,
+                             l.relu)
+        dt += time.perf_counter() - t0
+        flops += 2.0 * l.cin * l.cout * l.k * l.k * oh * ow * act
+        n += 1
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": "ResNet-50 layer1.0 (4 convs) at 256x512x64 bf16, dense-then-select in fp64, "
-                      f"{int((mask != 0).sum())}/{gh * gw} blocks active; {dt:.1f} s"}
+            "sample": f"ResNet-50 layer1 + layer2 ({n} convs) at their 2048x1024-frame sizes, bf16 "
+                      f"values, dense-then-select in fp64, {int((mask != 0).sum())}/{gh * gw} blocks "
+                      f"active; {dt:.1f} s"}
 
 
 def layer_sweep(torch, bc, dev):
@@ -257,9 +271,98 @@ def resnet18_clip(torch, dev, frames=30):
             "launch": "one HIP graph replay per sparse frame"}
 
 
-def rocprof_summary(path):
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "sparse_conv_traffic_resnet50_2048x1024_active0.3.txt")
+CONV_SOURCES = ("paper_2108_09376_amd/csrc/k_conv_mfma.hip", "paper_2108_09376_amd/csrc/bc_internal.h")
+
+
+def conv_source_sha():
+    """SHA-256 over the sparse-conv kernel sources: counters taken on other code are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in CONV_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def pmc_summary(fetch_csv, write_csv):
+    """Text summary of two rocprofv3 --pmc runs of `bench.py --pmc-frames N` (FETCH_SIZE,
+    then WRITE_SIZE; KiB per dispatch). Both counters are scaled by what they read for
+    the calibration kernel (float32 negation of 64 Mi elements: 256 MiB read, 256 MiB
+    written). Sparse-conv dispatches are grouped into frames of 53 launches; the first
+    frame runs every block, the others the 38-block grid."""
+    import csv
+
+    from paper_2108_09376_amd import resnet
+
+    def load(path, counter):
+        per = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = int(r["Dispatch_Id"])
+            name, v = r["Kernel_Name"], float(r["Counter_Value"])
+            per[d] = (name, per.get(d, (name, 0.0))[1] + v)
+        return [per[d] for d in sorted(per)]
+
+    out = []
+    res = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = load(path, counter)
+        cal = [v for n, v in rows if "neg" in n.lower()]
+        if not cal:
+            raise SystemExit(f"{path}: no calibration (neg) dispatch found")
+        factor = (256 << 10) / cal[-1]
+        conv = [v * factor * 1024 for n, v in rows if "k_conv_" in n]
+        if len(conv) % 53:
+            raise SystemExit(f"{path}: {len(conv)} conv dispatches is not a whole number of frames")
+        frames = [conv[i:i + 53] for i in range(0, len(conv), 53)]
+        res[counter] = (factor, cal[-1], frames)
+    layers = resnet.build_layers(50)
+    shapes = resnet.layer_shapes(layers, 1024, 2048)
+    algo = [b for b in resnet.conv_algo_bytes(layers, shapes, (8, 16), 38) if b is not None]
+    algo_full = [b for b in resnet.conv_algo_bytes(layers, shapes, (8, 16), 128) if b is not None]
+    names = [l.name for l in layers if l.kind == "conv"]
+    f_fac, f_raw, f_frames = res["FETCH_SIZE"]
+    w_fac, w_raw, w_frames = res["WRITE_SIZE"]
+    sparse_f = [sum(fr[i] for fr in f_frames[1:]) / len(f_frames[1:]) for i in range(53)]
+    sparse_w = [sum(fr[i] for fr in w_frames[1:]) / len(w_frames[1:]) for i in range(53)]
+    out.append(f"calibration: FETCH_SIZE read {f_raw:.0f} KiB for 262144 KiB (factor {f_fac:.4f}); "
+               f"WRITE_SIZE read {w_raw:.0f} KiB for 262144 KiB (factor {w_fac:.4f})")
+    out.append(f"{'layer':24s} {'fetch_MB':>9s} {'write_MB':>9s} {'hbm_MB':>9s} {'algo_MB':>9s} {'ratio':>6s}")
+    for i in range(53):
+        tot = sparse_f[i] + sparse_w[i]
+        out.append(f"{names[i]:24s} {sparse_f[i] / 1e6:9.3f} {sparse_w[i] / 1e6:9.3f} {tot / 1e6:9.3f} "
+                   f"{algo[i] / 1e6:9.3f} {tot / algo[i]:6.2f}")
+    tf, tw_, ta = sum(sparse_f), sum(sparse_w), sum(algo)
+    full = sum(f_frames[0]) + sum(w_frames[0])
+    out.append(f"sparse frame (38/128 blocks): fetch {tf / 1e6:.1f} MB, write {tw_ / 1e6:.1f} MB, "
+               f"total {(tf + tw_) / 1e6:.1f} MB vs algorithmic {ta / 1e6:.1f} MB (x{(tf + tw_) / ta:.2f})")
+    out.append(f"full frame (128/128 blocks): total {full / 1e6:.1f} MB vs algorithmic "
+               f"{sum(algo_full) / 1e6:.1f} MB (x{full / sum(algo_full):.2f})")
+    out.append(f"traffic_bytes_per_conv_launch={(tf + tw_) / 53:.0f}")
+    out.append(f"algo_bytes_per_conv_launch={ta / 53:.0f}")
+    out.append(f"conv_source_sha256={conv_source_sha()}")
+    return "\n".join(out)
+
+
+def recorded_traffic():
+    """HBM bytes per sparse-conv launch from the committed counter summary, or None if
+    it is missing or was taken on other kernel sources."""
+    try:
+        kv = dict(l.split("=", 1) for l in open(TRAFFIC_PROFILE).read().splitlines() if "=" in l
+                  and " " not in l.split("=", 1)[0])
+    except OSError:
+        return None
+    if kv.get("conv_source_sha256") != conv_source_sha():
+        return None
+    return float(kv["traffic_bytes_per_conv_launch"])
+
+
+def rocprof_summary(path, trace=None, first=0, count=0):
     """Text summary of a rocprofv3 kernel_stats.csv: per-kernel calls / average / total,
-    and the sparse-conv kernels (k_conv_*) pooled into one average launch duration."""
+    and the sparse-conv kernels (k_conv_*) pooled into one average launch duration. With
+    the kernel_trace.csv of the same run and a window of conv dispatches (ordinals among
+    k_conv dispatches in start order, as bench.py reports it), the window is pooled too."""
     import csv
     rows = list(csv.DictReader(open(path)))
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
@@ -276,13 +379,26 @@ def rocprof_summary(path):
     if conv_n:
         lines.append(f"sparse conv kernels pooled: {int(conv_n)} launches, average "
                      f"{conv_t / conv_n / 1e3:.2f} us per launch")
+    if trace:
+        tr = [r for r in csv.DictReader(open(trace)) if "k_conv_" in r["Kernel_Name"]]
+        tr.sort(key=lambda r: int(r["Start_Timestamp"]))
+        win = tr[first:first + count]
+        if len(win) != count:
+            raise SystemExit(f"{trace}: only {len(tr)} conv dispatches, window needs {first + count}")
+        d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in win]
+        lines.append(f"sparse conv dispatches {first}..{first + count - 1} (the per-layer timing phase): "
+                     f"{count} launches, average {sum(d) / count:.2f} us per launch")
     return "\n".join(lines)
 
 
 def main():
     args = parse()
     if args.rocprof_summary:
-        print(rocprof_summary(args.rocprof_summary))
+        a = args.rocprof_summary
+        print(rocprof_summary(a[0], *(a[1:2] + [int(v) for v in a[2:4]])))
+        return
+    if args.pmc_summary:
+        print(pmc_summary(*args.pmc_summary))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -309,11 +425,11 @@ def main():
     torch.cuda.synchronize()
 
     if args.pmc_frames:
-        a0 = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        a0 = torch.empty(64 << 20, dtype=torch.float32, device=dev)
         a1 = torch.empty_like(a0)
-        a0.fill_(1)
+        a0.fill_(1.0)
         torch.cuda.synchronize()
-        a1.copy_(a0)                      # calibration: 256 MiB read + 256 MiB written
+        torch.neg(a0, out=a1)             # calibration: 256 MiB read + 256 MiB written
         torch.cuda.synchronize()
         net.set_mask(masks_for(args.frac))
         for _ in range(args.pmc_frames):
@@ -327,6 +443,44 @@ def main():
             net.frame(x, sparse=True)
         torch.cuda.synchronize()
         return
+
+    # Per-launch durations of the dominant kernel (the sparse conv), measured first, right
+    # after frame 0: each conv layer is captured as a graph of `reps` back-to-back launches
+    # on the frame's index and timed with HIP events on the capture stream, so host-side
+    # marshalling is not counted. Every launch of this phase is timed or warms its graph,
+    # so a kernel trace of this command pools exactly these dispatches: conv dispatches
+    # [53, 53 + 53 * (reps + 3 * reps)) in launch order (frame 0 comes first).
+    mask = masks_for(args.frac)
+    active = int(mask.sum())
+    flops = net.conv_flops(active)
+    net.set_mask(mask)
+    from paper_2108_09376_amd import bc
+    bc.bc_build_block_index(net.mask, 1, net.grid, net.idx, net.count)
+    torch.cuda.synchronize()
+    conv_idx = [i for i, l in enumerate(net.layers) if l.kind == "conv"]
+    reps = 10
+    layer_us = {}
+    for i in conv_idx:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                net.run_layer(i, x, net.idx, net.count)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        layer_us[i] = e0.elapsed_time(e1) * 1e3 / (3 * reps)
+        del g
+    conv_total_us = sum(layer_us.values())
+    achieved = flops / (conv_total_us * 1e-6) / 1e12
+    per_launch_us = conv_total_us / len(conv_idx)
+    slowest = sorted(layer_us.items(), key=lambda kv: -kv[1])[:5]
+
+    conv_window = {"first": len(conv_idx), "count": len(conv_idx) * reps * 4}
 
     graph = None
     if not args.no_graph:
@@ -361,46 +515,13 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
-    mask = masks_for(args.frac)
-    active = int(mask.sum())
     ms = time_frames(args.frac, args.steps, args.warmup)
-    flops = net.conv_flops(active)
     value = flops / (ms * 1e-3) / 1e12
 
     sweep = {}
     for f in [float(v) for v in args.sweep.split(",") if v.strip()]:
         sweep[f"{f:g}"] = round(time_frames(f, max(10, args.steps // 2), 3), 4)
     sweep[f"{args.frac:g}"] = round(ms, 4)
-
-    # Per-launch durations of the dominant kernel (the sparse conv). Each conv layer is
-    # captured as a graph of `reps` back-to-back launches on the frame's index and timed
-    # with HIP events on the capture stream, so host-side marshalling is not counted.
-    net.set_mask(mask)
-    from paper_2108_09376_amd import bc
-    bc.bc_build_block_index(net.mask, 1, net.grid, net.idx, net.count)
-    torch.cuda.synchronize()
-    conv_idx = [i for i, l in enumerate(net.layers) if l.kind == "conv"]
-    reps = 10
-    layer_us = {}
-    for i in conv_idx:
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for _ in range(reps):
-                net.run_layer(i, x, net.idx, net.count)
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(3):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        layer_us[i] = e0.elapsed_time(e1) * 1e3 / (3 * reps)
-        del g
-    conv_total_us = sum(layer_us.values())
-    achieved = flops / (conv_total_us * 1e-6) / 1e12
-    per_launch_us = conv_total_us / len(conv_idx)
-    slowest = sorted(layer_us.items(), key=lambda kv: -kv[1])[:5]
 
     out = {
         "metric": "effective TFLOP/s on active blocks + ms/frame at 2048x1024, 30% active",
@@ -425,7 +546,10 @@ def main():
                      "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "avg_launch_us": round(per_launch_us, 3), "conv_us_per_frame": round(conv_total_us, 2),
-                     "traffic": None,
+                     "traffic": recorded_traffic(),
+                     "algo_bytes_per_launch": round(sum(b for b in resnet.conv_algo_bytes(
+                         net.layers, net.shapes, net.grid, active) if b) / len(conv_idx)),
+                     "trace_conv_dispatch_window": conv_window,
                      "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
     if not args.no_layer_sweep:

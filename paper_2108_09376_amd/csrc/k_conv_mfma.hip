@@ -34,6 +34,7 @@
 // 7x7 RGB stem): K is ordered (kernel row i, then the kw*Cin values of that row,
 // which are contiguous in a channels-last row), one MFMA k step per kernel row.
 #include <mutex>
+#include <map>
 #include <set>
 #include <type_traits>
 
@@ -419,32 +420,62 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
 //
 // The layers of ResNet backbones (1x1 and 3x3, stride 1 or 2) run here. At the
 // active fractions of sparse frames most layers have only a few workgroups per CU,
-// so time is set by how many dependent memory round trips a workgroup makes, not by
-// the matrix cores. This form therefore
+// so time is set by one workgroup's chain of dependent memory round trips and by the
+// per-CU issue rate of its loads and LDS traffic, not by the matrix cores. This form
+// therefore
 //  * loads the active count and the tile's block ids in one round trip (ids are
 //    read unconditionally; the index holds at least n*gh*gw entries);
-//  * keeps a D-deep ring of weight slices in registers: the slice of k step j+D is
-//    requested right after step j's slice is staged to LDS, so each request has D
-//    steps of matrix work to land (k step = one tap of one 32-channel chunk);
-//  * requests the next chunk's halo one chunk ahead (3x3: nine steps), or D steps
-//    ahead through its own register ring when every step is a new chunk (1x1);
+//  * 1x1: every k step is a new 32-channel chunk; halo and weights ride 4-deep
+//    register rings (the data of step j+4 is requested right after step j is staged
+//    to LDS), one barrier per step;
+//  * 3x3, SG = 1: a chunk is nine k steps (one per tap); the weights of all taps are
+//    requested a chunk ahead and staged one tap per barrier, the halo once per chunk;
+//  * 3x3, SG = 9: the halo and all nine weight slices of a chunk are staged under one
+//    barrier and whole chunks ride a 2-deep register ring (more LDS, fewer barriers:
+//    chosen for layers with few tiles, where LDS residency does not matter);
 //  * splits K over `ksplit` workgroups for layers with few output tiles: each slice
 //    stores its fp32 partial tile, and the last slice to finish (a per-tile counter)
 //    adds the partials in fixed slice order 0, 1, ... and runs the epilogue, so the
 //    result does not depend on arrival order. The counter is reset by that last
 //    workgroup, so no memset is needed between calls (safe under graph replay).
-// LDS: halo double buffer + weight double buffer, one barrier per k step.
+// The summation order over K (chunk by chunk, taps in order) is the same for every
+// stage grouping, so the grouping never changes results.
 
 constexpr int kMaxSplitTiles = 1 << 16;
 constexpr int kMaxSplit = 4;        // K slices per tile
 __device__ uint32_t g_split_counter[kMaxSplitTiles];   // zero at load, reset after use
 
-template <int BM, int KT>
+// Halo vectors (16 bytes) each thread stages per chunk: the halo of a 64-row tile has at
+// most 192 slots at stride 1 and 384 at stride 2 (a 128-row tile: 704). Every vector
+// costs a load instruction even when it falls outside the halo, so the bound is kept
+// tight per stride.
+template <int BM, int KT, int S>
 struct PipeShape {
-    static constexpr int AU = (KT == 1) ? BM / 64 : (BM == 64 ? 6 : 11);  // halo vectors / thread
+    static constexpr int AU = (KT == 1) ? BM / 64 : (BM == 64 ? (S == 1 ? 3 : 6) : 11);
 };
 
-template <bool BF16, int BM, int BN, int KS, int S, int D>
+// Ring of compile-time slots: calls f(integral_constant<I>, j + I) for I = 0 .. D-1 while
+// j + I < n, so every ring slot is a constant index in the step body it runs.
+template <int I, int D>
+struct RingSteps {
+    template <class F>
+    __device__ __forceinline__ static void run(F &f, int j, int n)
+    {
+        if (j + I < n) {
+            f(std::integral_constant<int, I>{}, j + I);
+            RingSteps<I + 1, D>::run(f, j, n);
+        }
+    }
+};
+template <int D>
+struct RingSteps<D, D> {
+    template <class F>
+    __device__ __forceinline__ static void run(F &, int, int) {}
+};
+
+// SG (stage grouping) sets how much of K one barrier covers: one tap (SG = 1) or all KT
+// taps of a 32-channel chunk (SG = KT, 3x3 layers only).
+template <bool BF16, int BM, int BN, int KS, int S, int SG>
 __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 {
     constexpr int SS = (KS == 1) ? S : 1;
@@ -453,7 +484,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int MI = WM / 16, NI = WN / 16;
     constexpr int BV = BN / 64;
-    constexpr int AU = PipeShape<BM, KT>::AU;
+    constexpr int AU = PipeShape<BM, KT, S>::AU;
     extern __shared__ __align__(16) uint8_t smem[];
     __shared__ TileBlocks tb;
     __shared__ int s_last;
@@ -490,7 +521,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
         for (int v = 0; v < BV; ++v)
             r[v] = bload(wr, ok ? wq + (64 * v * KT * a.cin + tap * a.cin + c * BK) * 2 : kOutOfRange);
     };
-    constexpr int RB = (KT == 1) ? D : KT;   // weight ring depth in k steps
+    static_assert(SG == 1 || (KT > 1 && SG == KT), "stage grouping: one tap, or every tap of a chunk");
     const int hrhc = a.HR * a.HC;
     const int aslot = ((a.nslot + 15) & ~15) * PITCH;
     uint8_t *sA = smem;
@@ -567,15 +598,15 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     Epilogue<BF16, BM, BN> epi;
     if constexpr (KT == 1) {
         // every k step is a new chunk: halo and weights ride D-deep register rings
+        constexpr int D = 4;
         uint4 ra[D][AU];
-        uint4 rb[RB][BV];
+        uint4 rb[D][BV];
 #pragma unroll
         for (int d = 0; d < D; ++d) {
             load_a(c_lo + d, ra[d]);
             load_b(d, rb[d]);
         }
         epi.prefetch(a, tb, n0);
-        // ring slot d is a compile-time index in every step body
         auto step = [&](auto dc, int j) {
             constexpr int d = decltype(dc)::value;
             uint8_t *sa = sA + (j & 1) * aslot;
@@ -587,22 +618,12 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
             load_a(c_lo + j + D, ra[d]);
             compute(sa, sb, 0);
         };
-        static_assert(D == 4, "the step sequence below is written for four ring slots");
-        int j = 0;
-        for (; j + 4 <= nsteps; j += 4) {
-            step(std::integral_constant<int, 0>{}, j);
-            step(std::integral_constant<int, 1>{}, j + 1);
-            step(std::integral_constant<int, 2>{}, j + 2);
-            step(std::integral_constant<int, 3>{}, j + 3);
-        }
-        if (j < nsteps) step(std::integral_constant<int, 0>{}, j);
-        if (j + 1 < nsteps) step(std::integral_constant<int, 1>{}, j + 1);
-        if (j + 2 < nsteps) step(std::integral_constant<int, 2>{}, j + 2);
-    } else {
+        for (int j = 0; j < nsteps; j += D) RingSteps<0, D>::run(step, j, nsteps);
+    } else if constexpr (SG == 1) {
         // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
         // while the current chunk is multiplied
         uint4 ra[AU];
-        uint4 rb[RB][BV];
+        uint4 rb[KT][BV];
         load_a(c_lo, ra);
 #pragma unroll
         for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
@@ -622,6 +643,36 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
                 compute(sa, sb, ((t / KS) * a.HC + (t % KS)) * PITCH);
             }
         }
+    } else {
+        // a stage is one chunk with every tap: its halo and all KT weight slices are
+        // staged under one barrier; chunks ride a 2-deep register ring and an LDS double
+        // buffer (sB holds KT slices per buffer)
+        constexpr int D = 2;
+        const int nch = c_hi - c_lo;
+        uint4 ra[D][AU];
+        uint4 rb[D][KT][BV];
+        auto load_stage = [&](int cj, uint4 (&xa)[AU], uint4 (&xb)[KT][BV]) {
+            load_a(c_lo + cj, xa);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) load_b(cj * KT + t, xb[t]);
+        };
+#pragma unroll
+        for (int d = 0; d < D; ++d) load_stage(d, ra[d], rb[d]);
+        epi.prefetch(a, tb, n0);
+        auto step = [&](auto dc, int cj) {
+            constexpr int d = decltype(dc)::value;
+            uint8_t *sa = sA + (cj & 1) * aslot;
+            uint8_t *sb = sB + (cj & 1) * KT * BN * PITCH;
+            store_a(sa, ra[d]);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) store_b(sb + t * BN * PITCH, rb[d][t]);
+            __syncthreads();
+            load_stage(cj + D, ra[d], rb[d]);
+#pragma unroll
+            for (int t = 0; t < KT; ++t)
+                compute(sa, sb + t * BN * PITCH, ((t / KS) * a.HC + (t % KS)) * PITCH);
+        };
+        for (int cj = 0; cj < nch; cj += D) RingSteps<0, D>::run(step, cj, nch);
     }
 
     if constexpr (BM == 64 && BN == 64) if (a.ksplit > 1) {
@@ -826,16 +877,25 @@ struct Plan {
     int BM, BN;
     Form form;
     MfmaArgs a;
+    int sg = 1;                // pipelined form: stage grouping (k_conv_pipe's SG)
+    unsigned tiles;            // output tiles of a full frame (before any K split)
     size_t lds;
     size_t ws_bytes;
     unsigned grid;
 };
 
-constexpr int kPipeStages = 4;
-constexpr size_t kMaxLdsPipe = 160 * 1024;
+constexpr size_t kMaxLdsPipe = 159 * 1024;   // 160 KB less room for static shared memory
 
 size_t epi_lds(int BM) { return (size_t)4 * (BM / 2) * EPITCH * sizeof(float); }
 size_t round16(size_t v) { return (v + 15) & ~(size_t)15; }
+
+// LDS of the pipelined form: double buffers of the halo and of the weight slices (SG per
+// buffer), or the epilogue scratch if larger.
+size_t pipe_lds(int nslot, int BM, int BN, int SG)
+{
+    const size_t main = 2 * round16(nslot) * PITCH + (size_t)2 * SG * BN * PITCH;
+    return main > epi_lds(BM) ? main : epi_lds(BM);
+}
 
 // Tiling of the output blocks into M tiles of BM rows; false if BM cannot take them.
 bool tile_rows(const LayerGeom &g, int BM, MfmaArgs &a)
@@ -854,7 +914,7 @@ bool tile_rows(const LayerGeom &g, int BM, MfmaArgs &a)
     return true;
 }
 
-int pipe_au(int BM, int KT) { return KT == 1 ? BM / 64 : (BM == 64 ? 6 : 11); }
+int pipe_au(int BM, int KT, int S) { return KT == 1 ? BM / 64 : (BM == 64 ? (S == 1 ? 3 : 6) : 11); }
 
 bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 {
@@ -890,9 +950,9 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
         a.rowpitch = 0;
         if (KS == 1 || KS == 3) {
             pl.form = Form::Pipe;
-            if (a.nslot > 64 * pipe_au(BM, KS * KS)) return false;
-            const size_t main = 2 * round16(a.nslot) * PITCH + (size_t)2 * BN * PITCH;
-            pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+            if (a.nslot > 64 * pipe_au(BM, KS * KS, S)) return false;
+            pl.sg = 1;
+            pl.lds = pipe_lds(a.nslot, BM, BN, 1);
             if (pl.lds > kMaxLdsPipe) return false;
         } else {
             pl.form = Form::General;
@@ -906,7 +966,8 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
     pl.BN = BN;
     a.ntn = g.cout / BN;
     const int mt_full = (a.P == 1) ? g.total_blocks * a.tpb : (g.total_blocks + a.P - 1) / a.P;
-    pl.grid = (unsigned)mt_full * a.ntn;
+    pl.tiles = (unsigned)mt_full * a.ntn;
+    pl.grid = pl.tiles;
     return true;
 }
 
@@ -933,6 +994,18 @@ bool choose_plan(const LayerGeom &g, Plan &best)
                 a.ksplit = (nchunk + a.cps - 1) / a.cps;
                 best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
                 best.grid = tiles * a.ksplit;
+            }
+            // Stage grouping (3x3): with at most 512 tiles on a full frame (the stride-16
+            // and stride-32 layers: few workgroups, long K) staging all nine taps of a
+            // chunk under one barrier is faster; with more tiles the smaller LDS footprint
+            // of one tap per barrier keeps more workgroups resident, which wins. SG does
+            // not change the summation order.
+            if (g.kh == 3 && best.BM == 64 && best.BN == 64 && best.tiles <= 512 && a.cps >= 2) {
+                const size_t lds = pipe_lds(a.nslot, best.BM, best.BN, 9);
+                if (lds <= kMaxLdsPipe) {
+                    best.sg = 9;
+                    best.lds = lds;
+                }
             }
             best.a.tiles_full = (int)best.grid;
             return true;
@@ -987,52 +1060,64 @@ hipError_t workspace(size_t bytes, float **out)
 }
 
 std::mutex g_attr_mu;
-std::set<const void *> g_attr_done;
+std::map<const void *, size_t> g_attr_lds;   // dynamic LDS each kernel has opted in to
 
 template <typename K>
-void launch_kernel(K kernel, const Plan &p, hipStream_t s)
+hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
 {
     if (p.lds > 64 * 1024) {
-        // opt in to more than 64 KB of LDS (gfx950 has 160 KB per workgroup), once per kernel
+        // opt in to more than 64 KB of dynamic LDS (gfx950: 160 KB per workgroup, static
+        // shared memory included), raised per kernel to the largest size launched so far
         std::lock_guard<std::mutex> lk(g_attr_mu);
-        if (g_attr_done.insert((const void *)kernel).second)
-            (void)hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      (int)kMaxLdsPipe);
+        size_t &cur = g_attr_lds[(const void *)kernel];
+        if (cur < p.lds) {
+            const hipError_t e = hipFuncSetAttribute(
+                (const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+            if (e != hipSuccess) return e;
+            cur = p.lds;
+        }
     }
     hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads), p.lds, s, p.a);
+    return hipSuccess;
 }
 
 template <bool BF16, int BM, int BN, int KS, int S>
-void launch_one(const Plan &p, hipStream_t s)
+hipError_t launch_one(const Plan &p, hipStream_t s)
 {
     if (p.form == Form::Stem) {
         if constexpr (BN == 64) {
-            if (p.a.cin <= 4) launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 4>, p, s);
-            else if constexpr (KS <= 4) launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 8>, p, s);
+            if (p.a.cin <= 4) return launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 4>, p, s);
+            else if constexpr (KS <= 4) return launch_kernel(k_conv_mfma_stem<BF16, BM, BN, KS, S, 8>, p, s);
         }
     } else if (p.form == Form::Pipe) {
-        if constexpr (KS == 1 || KS == 3) launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, kPipeStages>, p, s);
+        if constexpr (KS == 1 || KS == 3) {
+            // all-tap stages exist for the 64x64 tiles the planner gives them to
+                if constexpr (BM == 64 && BN == 64 && KS == 3)
+                if (p.sg == 9) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 9>, p, s);
+            if (p.sg == 1) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 1>, p, s);
+        }
     } else {
-        launch_kernel(k_conv_mfma<BF16, BM, BN, KS, S>, p, s);
+        return launch_kernel(k_conv_mfma<BF16, BM, BN, KS, S>, p, s);
     }
+    return hipErrorInvalidValue;   // no kernel for this plan
 }
 
 template <bool BF16, int KS, int S>
-void launch_tiles(const Plan &p, hipStream_t s)
+hipError_t launch_tiles(const Plan &p, hipStream_t s)
 {
-    if (p.BM == 128 && p.BN == 128) launch_one<BF16, 128, 128, KS, S>(p, s);
-    else if (p.BM == 128) launch_one<BF16, 128, 64, KS, S>(p, s);
-    else if (p.BN == 128) launch_one<BF16, 64, 128, KS, S>(p, s);
-    else launch_one<BF16, 64, 64, KS, S>(p, s);
+    if (p.BM == 128 && p.BN == 128) return launch_one<BF16, 128, 128, KS, S>(p, s);
+    if (p.BM == 128) return launch_one<BF16, 128, 64, KS, S>(p, s);
+    if (p.BN == 128) return launch_one<BF16, 64, 128, KS, S>(p, s);
+    return launch_one<BF16, 64, 64, KS, S>(p, s);
 }
 
 template <bool BF16>
-void launch_geom(const Plan &p, int ks, int stride, hipStream_t s)
+hipError_t launch_geom(const Plan &p, int ks, int stride, hipStream_t s)
 {
-    if (ks == 1) stride == 1 ? launch_tiles<BF16, 1, 1>(p, s) : launch_tiles<BF16, 1, 2>(p, s);
-    else if (ks == 3) stride == 1 ? launch_tiles<BF16, 3, 1>(p, s) : launch_tiles<BF16, 3, 2>(p, s);
-    else if (ks == 5) stride == 1 ? launch_tiles<BF16, 5, 1>(p, s) : launch_tiles<BF16, 5, 2>(p, s);
-    else stride == 1 ? launch_tiles<BF16, 7, 1>(p, s) : launch_tiles<BF16, 7, 2>(p, s);
+    if (ks == 1) return stride == 1 ? launch_tiles<BF16, 1, 1>(p, s) : launch_tiles<BF16, 1, 2>(p, s);
+    if (ks == 3) return stride == 1 ? launch_tiles<BF16, 3, 1>(p, s) : launch_tiles<BF16, 3, 2>(p, s);
+    if (ks == 5) return stride == 1 ? launch_tiles<BF16, 5, 1>(p, s) : launch_tiles<BF16, 5, 2>(p, s);
+    return stride == 1 ? launch_tiles<BF16, 7, 1>(p, s) : launch_tiles<BF16, 7, 2>(p, s);
 }
 
 }  // namespace
@@ -1103,8 +1188,9 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
         hipError_t e = workspace(p.ws_bytes, &a.ws);
         if (e != hipSuccess) return e;
     }
-    if (fmt == Half16::BF16) launch_geom<true>(p, g.kh, g.stride, s);
-    else launch_geom<false>(p, g.kh, g.stride, s);
+    const hipError_t e = fmt == Half16::BF16 ? launch_geom<true>(p, g.kh, g.stride, s)
+                                             : launch_geom<false>(p, g.kh, g.stride, s);
+    if (e != hipSuccess) return e;
     return hipGetLastError();
 }
 

@@ -93,6 +93,36 @@ def default_params(layers: list[Layer], seed0: int = 1000, bn_random: bool = Fal
     return out
 
 
+def layer_shapes(layers: list[Layer], h: int, w: int) -> list[tuple[int, int, int]]:
+    """(out_h, out_w, out_c) of every layer for an h x w frame (the dense conv formula)."""
+    shapes = []
+    for l in layers:
+        ih, iw = (h, w) if l.src < 0 else shapes[l.src][:2]
+        shapes.append(((ih + 2 * l.pad - l.k) // l.stride + 1,
+                       (iw + 2 * l.pad - l.k) // l.stride + 1, l.cout))
+    return shapes
+
+
+def conv_algo_bytes(layers: list[Layer], shapes, grid, active: int, esize: int = 2):
+    """Algorithmic HBM bytes of each convolution with `active` of the grid's blocks
+    executed: every element of the active blocks' input halo tiles read once, the
+    weights read once, the active output blocks (and residual blocks) read/written
+    once. Returns a list aligned with `layers` (None for non-conv layers)."""
+    gh, gw = grid
+    out = []
+    for l, (oh, ow, co) in zip(layers, shapes):
+        if l.kind != "conv":
+            out.append(None)
+            continue
+        bh, bw = oh // gh, ow // gw
+        th, tw = (bh - 1) * l.stride + l.k, (bw - 1) * l.stride + l.k
+        halo = active * th * tw * l.cin * esize
+        wts = l.cout * l.k * l.k * l.cin * esize + l.cout * 4
+        outb = active * bh * bw * co * esize
+        out.append(halo + wts + outb * (2 if l.res is not None else 1))
+    return out
+
+
 class SparseResNet:
     """ResNet backbone executed block-sparsely frame by frame.
 
@@ -111,12 +141,7 @@ class SparseResNet:
         self.dtype, self.device = dtype, torch.device(device)
         dcode = bc.BC_BF16 if dtype == torch.bfloat16 else bc.BC_F16
         params = params if params is not None else default_params(self.layers, seed0, bn_random)
-        self.shapes = []
-        for l in self.layers:
-            ih, iw = (h, w) if l.src < 0 else self.shapes[l.src][:2]
-            oh = (ih + 2 * l.pad - l.k) // l.stride + 1
-            ow = (iw + 2 * l.pad - l.k) // l.stride + 1
-            self.shapes.append((oh, ow, l.cout))
+        self.shapes = layer_shapes(self.layers, h, w)
         self.weights, self.biases = [], []
         for l, p in zip(self.layers, params):
             if l.kind != "conv":
