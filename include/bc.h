@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 1
+#define BC_ABI_VERSION 2
 
 typedef enum {
     BC_OK = 0,
@@ -212,6 +212,83 @@ bc_status bc_buffer_invalidate(bc_buffer b);
 bc_status bc_buffer_mark_written(bc_buffer b, int32_t full_mask);
 /* 1 if valid, 0 if not, -1 for a NULL or unknown handle. */
 int32_t bc_buffer_is_valid(bc_buffer b);
+
+/* ------------------------------------------------------------------------------
+ * Steps around the block-sparse network: execution decisions, frame state,
+ * information gain and rewards (Sections 3.3 to 3.5).
+ * ------------------------------------------------------------------------------ */
+
+/*
+ * Execution decisions sampled from the policy's block probabilities, fused with the
+ * index build (Section 3.5: P_t holds p_b in [0, 1] per block; A_t = [a_b] is drawn
+ * from it stochastically rather than by a threshold). The paper names no generator;
+ * this library uses Philox4x32-10 (Salmon et al., SC 2011): block b (raster id, as in
+ * the index) draws the first output word x of counter (b, frame mod 2^32,
+ * frame div 2^32, 0) under key (seed mod 2^32, seed div 2^32), u_b = (x >> 8) * 2^-24,
+ * and a_b = 1 exactly when u_b < p_b (fp32 compare; a NaN probability gives 0). The
+ * same (seed, frame, probabilities) always give the same grid.
+ *   d_prob   float32 [n][grid_h][grid_w], device.
+ *   d_mask   uint8 [n][grid_h][grid_w], device, written with a_b (0 or 1).
+ *   d_idx, d_count, h_count: as bc_build_block_index (ascending ids of a_b = 1).
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE (n, grid <= 0 or more than 2^20 blocks),
+ * BC_ERR_CAPACITY, BC_ERR_ALIAS (outputs overlapping each other or d_prob), BC_ERR_HIP.
+ */
+bc_status bc_sample_execution_grid(const float *d_prob, int32_t n, bc_grid g, uint64_t seed,
+                                   uint64_t frame, uint8_t *d_mask, int32_t *d_idx,
+                                   int32_t capacity, int32_t *d_count, int32_t *h_count,
+                                   void *stream);
+
+/*
+ * Frame-state update (Section 3.3: the previous frame state H_{t-1} is an RGB frame
+ * whose every block holds the image content of the last executed block there):
+ *   d_state[block] = d_frame[block] for the active blocks (a bit copy),
+ *   every other element of d_state untouched.
+ *   desc     shape/format of both tensors (any dtype, NCHW or NHWC); blocks are
+ *            desc.h / grid_h x desc.w / grid_w.
+ * d_idx/d_count may both be NULL (every block: the first frame of a clip).
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE,
+ * BC_ERR_CAPACITY, BC_ERR_ALIAS (frame and state overlap), BC_ERR_HIP.
+ */
+bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor desc, bc_grid g,
+                                const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                void *stream);
+
+/*
+ * Information gain for semantic segmentation (Section 3.4): per output pixel the KL
+ * divergence KL(O_t || O_{t-1}) between the class distributions of frame t and frame
+ * t-1, O = softmax over classes of the network's per-class scores; per block the
+ * maximum over its pixels (Eq. 1):
+ *   d_ig[n][gy][gx] = max over pixels p of block (gy, gx) of
+ *                     sum_c O_t[c,p] (log O_t[c,p] - log O_{t-1}[c,p]).
+ * Arithmetic: fp32 (log-sum-exp with the per-pixel maximum subtracted); a per-pixel
+ * value below zero (rounding, the exact KL is >= 0) counts as 0.
+ *   d_logits, d_prev_logits  float32 [n][c][h][w] (desc: F32, NCHW, 1 <= c <= 32).
+ *   d_ig     float32 [n][grid_h][grid_w], device (written completely).
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE,
+ * BC_ERR_ALIAS (d_ig overlapping an input), BC_ERR_UNSUPPORTED (c > 32), BC_ERR_HIP.
+ */
+bc_status bc_seg_information_gain(const float *d_logits, const float *d_prev_logits,
+                                  bc_tensor desc, bc_grid g, float *d_ig, void *stream);
+
+/*
+ * Block rewards and the policy loss (Section 3.5), per image n of the batch:
+ *   C_t = (number of executed blocks) / (grid_h * grid_w);
+ *   M_t = (1 - mu) * C_t + mu * M_{t-1}        (moving average of the cost);
+ *   R_b = (a_b ? IG_b : -IG_b) + gamma * (a_b ? tau - M_t : -(tau - M_t));
+ *   L   = -sum_b R_b * log(a_b ? p_b : 1 - p_b)   (REINFORCE).
+ *   d_ig      float32 [n][grid_h][grid_w] (bc_seg_information_gain's output).
+ *   d_mask    uint8 [n][grid_h][grid_w], nonzero = executed.
+ *   d_prob    float32 [n][grid_h][grid_w] or NULL (then no loss is computed).
+ *   d_mavg    float32 [n], device, in: M_{t-1}, out: M_t (the caller's state).
+ *   d_reward  float32 [n][grid_h][grid_w], device, written.
+ *   d_cost    float32 [n] or NULL: C_t.   d_loss  float32 [n] or NULL: L (needs d_prob).
+ * Arithmetic fp32; sums in a fixed order (the result does not depend on scheduling).
+ * Errors: BC_ERR_NULL (d_ig, d_mask, d_mavg, d_reward; d_loss without d_prob),
+ * BC_ERR_SHAPE, BC_ERR_ALIAS (outputs overlapping each other or an input), BC_ERR_HIP.
+ */
+bc_status bc_block_rewards(const float *d_ig, const uint8_t *d_mask, const float *d_prob,
+                           int32_t n, bc_grid g, float tau, float gamma, float mu, float *d_mavg,
+                           float *d_reward, float *d_cost, float *d_loss, void *stream);
 
 #ifdef __cplusplus
 }

@@ -68,6 +68,11 @@ _sigs = {
     "bc_buffer_invalidate": ([_vp], _i32),
     "bc_buffer_mark_written": ([_vp, _i32], _i32),
     "bc_buffer_is_valid": ([_vp], _i32),
+    "bc_sample_execution_grid": ([_vp, _i32, bc_grid, ctypes.c_uint64, ctypes.c_uint64, _vp, _vp, _i32,
+                                  _vp, _vp, _vp], _i32),
+    "bc_update_frame_state": ([_vp, _vp, bc_tensor, bc_grid, _vp, _vp, _i32, _vp], _i32),
+    "bc_seg_information_gain": ([_vp, _vp, bc_tensor, bc_grid, _vp, _vp], _i32),
+    "bc_block_rewards": ([_vp, _vp, _vp, _i32, bc_grid, _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
     _fn = getattr(_lib, _name)
@@ -187,6 +192,47 @@ def bc_sparse_maxpool2d(geom, x, layout, out, grid, idx, count, stream=None):
                                   desc(out, layout), _grid(grid), _ptr(idx), _ptr(count), cap,
                                   _stream(stream))
     _check(st, "bc_sparse_maxpool2d")
+
+
+def bc_sample_execution_grid(prob, grid, seed, frame, mask, idx, count, h_count=None, stream=None):
+    """prob float32 [n, gh, gw] (device) -> mask uint8 [n, gh, gw], idx int32 [capacity],
+    count int32 [1] (device). With h_count=True the count is also returned (synchronising)."""
+    hc = ctypes.c_int32(0) if h_count else None
+    st = _lib.bc_sample_execution_grid(_ptr(prob), int(prob.shape[0]), _grid(grid),
+                                       ctypes.c_uint64(int(seed)), ctypes.c_uint64(int(frame)),
+                                       _ptr(mask), _ptr(idx), int(idx.numel()), _ptr(count),
+                                       ctypes.byref(hc) if hc is not None else None, _stream(stream))
+    _check(st, "bc_sample_execution_grid")
+    return hc.value if hc is not None else None
+
+
+def bc_update_frame_state(frame, state, layout, grid, idx, count, stream=None):
+    """state[active blocks] = frame[active blocks]; frame/state same shape and dtype."""
+    if frame.shape != state.shape or frame.dtype != state.dtype:
+        raise ValueError("frame and state must have the same shape and dtype")
+    cap = 0 if idx is None else int(idx.numel())
+    st = _lib.bc_update_frame_state(_ptr(frame), _ptr(state), desc(state, layout), _grid(grid),
+                                    _ptr(idx), _ptr(count), cap, _stream(stream))
+    _check(st, "bc_update_frame_state")
+
+
+def bc_seg_information_gain(logits, prev_logits, grid, ig, stream=None):
+    """logits, prev_logits float32 [n, classes, h, w] -> ig float32 [n, gh, gw]."""
+    if logits.shape != prev_logits.shape:
+        raise ValueError("score maps must have the same shape")
+    st = _lib.bc_seg_information_gain(_ptr(logits), _ptr(prev_logits), desc(logits, BC_NCHW),
+                                      _grid(grid), _ptr(ig), _stream(stream))
+    _check(st, "bc_seg_information_gain")
+
+
+def bc_block_rewards(ig, mask, prob, grid, tau, gamma, mu, mavg, reward, cost=None, loss=None,
+                     stream=None):
+    """Rewards per block (reward [n, gh, gw]), C_t (cost [n]), M_t (mavg [n], in/out) and
+    the REINFORCE loss (loss [n], needs prob). All float32 device tensors, mask uint8."""
+    st = _lib.bc_block_rewards(_ptr(ig), _ptr(mask), _ptr(prob), int(ig.shape[0]), _grid(grid),
+                               float(tau), float(gamma), float(mu), _ptr(mavg), _ptr(reward),
+                               _ptr(cost), _ptr(loss), _stream(stream))
+    _check(st, "bc_block_rewards")
 
 
 def _np_ptr(a):

@@ -501,4 +501,112 @@ int32_t bc_buffer_is_valid(bc_buffer b)
     return b->valid;
 }
 
+// ---------------------------------------------------------------- policy-side steps
+
+bc_status bc_sample_execution_grid(const float *d_prob, int32_t n, bc_grid g, uint64_t seed,
+                                   uint64_t frame, uint8_t *d_mask, int32_t *d_idx,
+                                   int32_t capacity, int32_t *d_count, int32_t *h_count,
+                                   void *stream)
+{
+    if (!d_prob || !d_mask || !d_idx || !d_count)
+        return fail(BC_ERR_NULL, "d_prob, d_mask, d_idx and d_count are required");
+    if (n <= 0 || g.grid_h <= 0 || g.grid_w <= 0)
+        return fail(BC_ERR_SHAPE, "n and grid must be positive");
+    const double total = (double)n * g.grid_h * g.grid_w;
+    if (total > (double)(1 << 20)) return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    if (capacity < (int)total)
+        return fail(BC_ERR_CAPACITY, "capacity %d < n*grid_h*grid_w = %d", capacity, (int)total);
+    const size_t nb = (size_t)total;
+    if (overlap(d_idx, (size_t)capacity * 4, d_count, 4) || overlap(d_mask, nb, d_idx, (size_t)capacity * 4) ||
+        overlap(d_mask, nb, d_count, 4) || overlap(d_prob, nb * 4, d_mask, nb) ||
+        overlap(d_prob, nb * 4, d_idx, (size_t)capacity * 4) || overlap(d_prob, nb * 4, d_count, 4))
+        return fail(BC_ERR_ALIAS, "probabilities, mask, index and count must not overlap");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = bc::launch_sample_index(d_prob, (int)total, seed, frame, d_mask, d_idx, d_count, s);
+    if (e != hipSuccess) return hip_fail(e, "sampling launch");
+    if (h_count) {
+        e = hipMemcpyAsync(h_count, d_count, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "count copy");
+    }
+    return ok();
+}
+
+bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor desc, bc_grid g,
+                                const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                void *stream)
+{
+    if (!d_frame || !d_state) return fail(BC_ERR_NULL, "d_frame and d_state are required");
+    bc_status st = check_tensor(desc, "desc");
+    if (st) return st;
+    LayerGeom L;
+    if ((st = block_geom(desc, g, L))) return st;
+    if ((st = check_index(d_idx, d_count, capacity, L.total_blocks))) return st;
+    const size_t bytes = tensor_bytes(desc);
+    if (overlap(d_frame, bytes, d_state, bytes)) return fail(BC_ERR_ALIAS, "frame and state overlap");
+    if (d_idx && (overlap(d_idx, (size_t)capacity * 4, d_state, bytes) || overlap(d_count, 4, d_state, bytes)))
+        return fail(BC_ERR_ALIAS, "the index overlaps the state");
+    hipError_t e = bc::launch_frame_state(d_frame, d_state, desc.n, desc.c, desc.h, desc.w,
+                                          esize_of(desc.dtype), desc.layout == BC_NHWC, g.grid_h,
+                                          g.grid_w, d_idx, d_count, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "frame state launch");
+    return ok();
+}
+
+bc_status bc_seg_information_gain(const float *d_logits, const float *d_prev_logits,
+                                  bc_tensor desc, bc_grid g, float *d_ig, void *stream)
+{
+    if (!d_logits || !d_prev_logits || !d_ig)
+        return fail(BC_ERR_NULL, "d_logits, d_prev_logits and d_ig are required");
+    bc_status st = check_tensor(desc, "desc");
+    if (st) return st;
+    if (desc.dtype != BC_F32) return fail(BC_ERR_DTYPE, "scores must be float32");
+    if (desc.layout != BC_NCHW) return fail(BC_ERR_LAYOUT, "scores must be NCHW ([n][classes][h][w])");
+    LayerGeom L;
+    if ((st = block_geom(desc, g, L))) return st;
+    if (desc.c > 32) return fail(BC_ERR_UNSUPPORTED, "at most 32 classes (got %d)", desc.c);
+    const double img_bytes = 4.0 * desc.c * desc.h * desc.w;
+    if (img_bytes >= 2147483392.0) return fail(BC_ERR_UNSUPPORTED, "one image's scores must be < 2 GiB");
+    const size_t bytes = tensor_bytes(desc), igb = (size_t)L.total_blocks * 4;
+    if (overlap(d_ig, igb, d_logits, bytes) || overlap(d_ig, igb, d_prev_logits, bytes))
+        return fail(BC_ERR_ALIAS, "d_ig overlaps an input");
+    hipError_t e = bc::launch_seg_information_gain(d_logits, d_prev_logits, desc.n, desc.c, desc.h,
+                                                   desc.w, g.grid_h, g.grid_w, d_ig, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "information gain launch");
+    return ok();
+}
+
+bc_status bc_block_rewards(const float *d_ig, const uint8_t *d_mask, const float *d_prob,
+                           int32_t n, bc_grid g, float tau, float gamma, float mu, float *d_mavg,
+                           float *d_reward, float *d_cost, float *d_loss, void *stream)
+{
+    if (!d_ig || !d_mask || !d_mavg || !d_reward)
+        return fail(BC_ERR_NULL, "d_ig, d_mask, d_mavg and d_reward are required");
+    if (d_loss && !d_prob) return fail(BC_ERR_NULL, "the loss needs d_prob");
+    if (n <= 0 || g.grid_h <= 0 || g.grid_w <= 0)
+        return fail(BC_ERR_SHAPE, "n and grid must be positive");
+    const double total = (double)n * g.grid_h * g.grid_w;
+    if (total > (double)(1 << 20)) return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    const size_t nb = (size_t)total;
+    const void *outs[4] = {d_mavg, d_reward, d_cost, d_loss};
+    const size_t outb[4] = {(size_t)n * 4, nb * 4, (size_t)n * 4, (size_t)n * 4};
+    const void *ins[3] = {d_ig, d_mask, d_prob};
+    const size_t inb[3] = {nb * 4, nb, nb * 4};
+    for (int i = 0; i < 4; ++i) {
+        for (int j = 0; j < 3; ++j)
+            if (i > 0 && overlap(outs[i], outb[i], ins[j], inb[j]))   // d_mavg is in/out
+                return fail(BC_ERR_ALIAS, "an output overlaps an input");
+        for (int j = i + 1; j < 4; ++j)
+            if (overlap(outs[i], outb[i], outs[j], outb[j]))
+                return fail(BC_ERR_ALIAS, "outputs overlap each other");
+    }
+    for (int j = 0; j < 3; ++j)
+        if (overlap(d_mavg, (size_t)n * 4, ins[j], inb[j]))
+            return fail(BC_ERR_ALIAS, "d_mavg overlaps an input");
+    hipError_t e = bc::launch_block_rewards(d_ig, d_mask, d_prob, n, g.grid_h * g.grid_w, tau, gamma,
+                                            mu, d_mavg, d_reward, d_cost, d_loss, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "rewards launch");
+    return ok();
+}
+
 }  // extern "C"

@@ -47,4 +47,19 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
 // Host-side check used by the ABI validation before anything is enqueued.
 bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why);
 
+// Execution decisions from block probabilities (Philox4x32-10) fused with the index.
+hipError_t launch_sample_index(const float *prob, int total, uint64_t seed, uint64_t frame,
+                               uint8_t *mask, int32_t *idx, int32_t *count, hipStream_t s);
+// Frame state: copy the active blocks of `frame` into `state` (same shape, any dtype).
+hipError_t launch_frame_state(const void *frame, void *state, int n, int c, int h, int w,
+                              int esize, bool nhwc, int gh, int gw, const int32_t *idx,
+                              const int32_t *count, hipStream_t s);
+// Per-block maximum of the per-pixel KL divergence of two [n][c][h][w] score maps.
+hipError_t launch_seg_information_gain(const float *lt, const float *lp, int n, int c, int h,
+                                       int w, int gh, int gw, float *ig, hipStream_t s);
+// Rewards, cost, moving average and REINFORCE loss per image.
+hipError_t launch_block_rewards(const float *ig, const uint8_t *mask, const float *prob, int n,
+                                int blocks, float tau, float gamma, float mu, float *mavg,
+                                float *reward, float *cost, float *loss, hipStream_t s);
+
 }  // namespace bc

@@ -234,3 +234,39 @@ class SyntheticClip:
             for (y, x, rh, rw) in pos:
                 m[y // b:(y + rh - 1) // b + 1, x // b:(x + rw - 1) // b + 1] = 1
         return m[None]
+
+
+# ---------------------------------------------------------------- policy-side inputs
+
+def seg_logits(r: np.random.Generator, n: int, classes: int, h: int, w: int,
+               scale: float = 4.0, cell: int = 16) -> np.ndarray:
+    """Per-class segmentation scores with spatial structure, standing in for a
+    segmentation network's output on a Cityscapes frame (19 classes at full 2048x1024
+    resolution): a coarse random field (one value per cell x cell patch) repeated over
+    its patch, plus fine N(0, 0.5) noise. float32 [n, classes, h, w]."""
+    ch, cw = -(-h // cell), -(-w // cell)
+    coarse = r.normal(0.0, scale, (n, classes, ch, cw)).astype(np.float32)
+    f = np.repeat(np.repeat(coarse, cell, axis=2), cell, axis=3)[:, :, :h, :w]
+    return (f + r.normal(0.0, 0.5, (n, classes, h, w)).astype(np.float32)).astype(np.float32)
+
+
+def seg_logits_next(r: np.random.Generator, prev: np.ndarray, changed: float = 0.25,
+                    cell: int = 64, scale: float = 4.0) -> np.ndarray:
+    """The next frame's scores: a random fraction `changed` of the cell x cell patches
+    get new scores (moving content), every other pixel keeps its scores plus small
+    N(0, 0.05) noise. float32, same shape as prev."""
+    n, c, h, w = prev.shape
+    out = prev + r.normal(0.0, 0.05, prev.shape).astype(np.float32)
+    ch, cw = -(-h // cell), -(-w // cell)
+    pick = r.random((n, ch, cw)) < changed
+    for img, cy, cx in zip(*np.nonzero(pick)):
+        ys, xs = slice(cy * cell, min(h, cy * cell + cell)), slice(cx * cell, min(w, cx * cell + cell))
+        out[img, :, ys, xs] = r.normal(0.0, scale, (c, 1, 1)) + r.normal(0.0, 0.5, out[img, :, ys, xs].shape)
+    return out.astype(np.float32)
+
+
+def block_probabilities(r: np.random.Generator, n: int, gh: int, gw: int) -> np.ndarray:
+    """Policy outputs p_b in [0, 1] per block: a mix of confident (near 0 or 1) and
+    uncertain blocks, as a trained policy produces. float32 [n, gh, gw]."""
+    p = r.beta(0.4, 0.8, (n, gh, gw))
+    return p.astype(np.float32)

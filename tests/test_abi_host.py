@@ -27,7 +27,9 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ["bc_build_block_index", "bc_sparse_conv2d", "bc_gather_halo", "bc_scatter_blocks",
               "bc_sparse_maxpool2d", "bc_fold_bn", "bc_buffer_register", "bc_buffer_release",
-              "bc_buffer_invalidate", "bc_buffer_mark_written", "bc_buffer_is_valid"]:
+              "bc_buffer_invalidate", "bc_buffer_mark_written", "bc_buffer_is_valid",
+              "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
+              "bc_block_rewards"]:
         assert n in names
 
 
@@ -36,7 +38,7 @@ def test_library_exports_every_declared_symbol(B):
     for n in declared_functions():
         assert hasattr(lib, n), n
     assert set(B.EXPORTED) == set(declared_functions())
-    assert B.bc_abi_version() == 1
+    assert B.bc_abi_version() == 2
     # and the symbols are plain C (unmangled)
     out = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
     for n in declared_functions():
@@ -137,6 +139,46 @@ def test_gather_scatter_pool_validation_codes(B):
     assert lib.bc_sparse_maxpool2d(ctypes.byref(pc), FAKE_IN, pin, FAKE_OUT, B.bc_tensor(1, 32, 256, 512, 1, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_SHAPE
     assert lib.bc_sparse_maxpool2d(ctypes.byref(pc), FAKE_IN, pin, FAKE_OUT, B.bc_tensor(1, 64, 255, 512, 1, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_SHAPE
     assert lib.bc_sparse_maxpool2d(ctypes.byref(pc), FAKE_IN, B.bc_tensor(1, 12, 512, 1024, 1, 1), FAKE_OUT, B.bc_tensor(1, 12, 256, 512, 1, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_UNSUPPORTED
+
+
+@no_gpu
+def test_policy_step_validation_codes(B):
+    lib = B.raw()
+    g = B.bc_grid(8, 16)
+    u64 = ctypes.c_uint64
+    # sampling fused with the index
+    assert lib.bc_sample_execution_grid(None, 1, g, u64(1), u64(0), FAKE_OUT, FAKE_IDX, 128, FAKE_CNT, None, None) == B.BC_ERR_NULL
+    assert lib.bc_sample_execution_grid(FAKE_IN, 1, g, u64(1), u64(0), None, FAKE_IDX, 128, FAKE_CNT, None, None) == B.BC_ERR_NULL
+    assert lib.bc_sample_execution_grid(FAKE_IN, 1, g, u64(1), u64(0), FAKE_OUT, FAKE_IDX, 127, FAKE_CNT, None, None) == B.BC_ERR_CAPACITY
+    assert lib.bc_sample_execution_grid(FAKE_IN, 0, g, u64(1), u64(0), FAKE_OUT, FAKE_IDX, 128, FAKE_CNT, None, None) == B.BC_ERR_SHAPE
+    assert lib.bc_sample_execution_grid(FAKE_IN, 1, g, u64(1), u64(0), FAKE_IN + 64, FAKE_IDX, 128, FAKE_CNT, None, None) == B.BC_ERR_ALIAS
+    # frame state
+    d = B.bc_tensor(1, 3, 1024, 2048, 1, 1)
+    assert lib.bc_update_frame_state(None, FAKE_OUT, d, g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_NULL
+    assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, d, g, FAKE_IDX, None, 128, None) == B.BC_ERR_NULL
+    assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, d, B.bc_grid(7, 16), FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_NOT_DIVISIBLE
+    assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, d, g, FAKE_IDX, FAKE_CNT, 100, None) == B.BC_ERR_CAPACITY
+    assert lib.bc_update_frame_state(FAKE_IN, FAKE_IN + 1024, d, g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_ALIAS
+    assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, B.bc_tensor(1, 3, 1024, 2048, 7, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_DTYPE
+    # information gain
+    sc = B.bc_tensor(1, 19, 1024, 2048, 0, 0)
+    assert lib.bc_seg_information_gain(FAKE_IN, None, sc, g, FAKE_OUT, None) == B.BC_ERR_NULL
+    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 19, 1024, 2048, 1, 0), g, FAKE_OUT, None) == B.BC_ERR_DTYPE
+    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 19, 1024, 2048, 0, 1), g, FAKE_OUT, None) == B.BC_ERR_LAYOUT
+    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 33, 1024, 2048, 0, 0), g, FAKE_OUT, None) == B.BC_ERR_UNSUPPORTED
+    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, sc, B.bc_grid(3, 16), FAKE_OUT, None) == B.BC_ERR_NOT_DIVISIBLE
+    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, sc, g, FAKE_W + 64, None) == B.BC_ERR_ALIAS
+    # rewards
+    f = ctypes.c_float
+    args = lambda **kw: [kw.get(k, v) for k, v in [("ig", FAKE_IN), ("mask", FAKE_W), ("prob", FAKE_RES), ("n", 1), ("g", g),
+                                                    ("tau", f(0.3)), ("gamma", f(5.0)), ("mu", f(0.9)), ("mavg", FAKE_IDX),
+                                                    ("reward", FAKE_OUT), ("cost", None), ("loss", FAKE_CNT), ("s", None)]]
+    assert lib.bc_block_rewards(*args(ig=None)) == B.BC_ERR_NULL
+    assert lib.bc_block_rewards(*args(prob=None)) == B.BC_ERR_NULL            # loss without prob
+    assert lib.bc_block_rewards(*args(n=0)) == B.BC_ERR_SHAPE
+    assert lib.bc_block_rewards(*args(reward=FAKE_IN + 16)) == B.BC_ERR_ALIAS
+    assert lib.bc_block_rewards(*args(loss=FAKE_OUT + 4)) == B.BC_ERR_ALIAS
+    assert B.bc_last_error()
 
 
 @no_gpu
