@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-scatter", action="store_true")
     ap.add_argument("--no-clip", action="store_true", help="skip the ResNet-18 30-frame clip")
+    ap.add_argument("--no-policy-steps", action="store_true",
+                    help="skip sampling / frame state / information gain / rewards")
     ap.add_argument("--pmc-frames", type=int, default=0,
                     help="rocprofv3 --pmc helper: a 256 MiB float32 negation (calibration) then N sparse frames "
                          "at --frac launched layer by layer; prints nothing else")
@@ -219,6 +221,73 @@ def gather_scatter(torch, bc, dev):
                                    "cold_GBps": round(nbytes / cold_us / 1e3, 1),
                                    "cold_frac_of_hbm_peak": round(nbytes / cold_us / 1e3 / PEAK_HBM_GBS, 3)}
             del g
+    return out
+
+
+def policy_steps(torch, bc, dev):
+    """The steps around the network at the workload's sizes (2048x1024 frame, 8x16 grid
+    of 128-px blocks, 38 blocks active where a grid is given), each timed as a captured
+    graph of 10 launches (5 replays):
+      sample_grid       execution decisions from 128 block probabilities + index
+      frame_state       executed blocks of the bf16 RGB frame copied into the state;
+                        algorithmic bytes = 38 blocks x 128x128x3 x 2 B, read + written
+      seg_information_gain  19-class fp32 scores of frame t and t-1 (2 x 159 MB read,
+                        more than the 256 MB last-level cache holds), per-pixel KL and
+                        block max; algorithmic bytes = both score maps once
+      block_rewards     rewards, cost, moving average and loss over 128 blocks"""
+    import numpy as np
+
+    import synth
+    r = synth.rng(7)
+    prob = torch.from_numpy(synth.block_probabilities(r, 1, 8, 16)).to(dev)
+    mask = torch.empty((1, 8, 16), dtype=torch.uint8, device=dev)
+    idx = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    m38 = torch.from_numpy(synth.frac_mask(synth.SEED_MASK0 + 1, 8, 16, 0.3)).to(dev)
+    idx38 = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt38 = torch.empty(1, dtype=torch.int32, device=dev)
+    bc.bc_build_block_index(m38, 1, (8, 16), idx38, cnt38)
+    frame = torch.randn((1, 1024, 2048, 3), device=dev).to(torch.bfloat16)
+    state = torch.zeros_like(frame)
+    lt = torch.from_numpy(synth.seg_logits(r, 1, 19, 1024, 2048)).to(dev)
+    lp = (lt + 0.1 * torch.randn_like(lt)).contiguous()
+    ig = torch.empty((1, 8, 16), dtype=torch.float32, device=dev)
+    mavg = torch.full((1,), 0.3, device=dev)
+    reward = torch.empty((1, 8, 16), device=dev)
+    cost = torch.empty(1, device=dev)
+    loss = torch.empty(1, device=dev)
+    ops = {
+        "sample_grid": (lambda: bc.bc_sample_execution_grid(prob, (8, 16), 2021, 5, mask, idx, cnt), None),
+        "frame_state": (lambda: bc.bc_update_frame_state(frame, state, bc.BC_NHWC, (8, 16), idx38, cnt38),
+                        2 * 38 * 128 * 128 * 3 * 2),
+        "seg_information_gain": (lambda: bc.bc_seg_information_gain(lt, lp, (8, 16), ig),
+                                 2 * 19 * 1024 * 2048 * 4),
+        "block_rewards": (lambda: bc.bc_block_rewards(ig, mask, prob, (8, 16), 0.3, 5.0, 0.9, mavg, reward,
+                                                      cost, loss), None),
+    }
+    out = {}
+    for name, (fn, nbytes) in ops.items():
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / 50
+        row = {"us": round(us, 2)}
+        if nbytes:
+            row.update({"bytes": nbytes, "GBps": round(nbytes / us / 1e3, 1),
+                        "frac_of_hbm_peak": round(nbytes / us / 1e3 / PEAK_HBM_GBS, 3)})
+        out[name] = row
+        del g
     return out
 
 
@@ -558,6 +627,8 @@ def main():
         out["gather_scatter"] = gather_scatter(torch, bc, dev)
     if not args.no_clip:
         out["resnet18_clip"] = resnet18_clip(torch, dev)
+    if not args.no_policy_steps:
+        out["policy_steps"] = policy_steps(torch, bc, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mask)
     print(json.dumps(out))
