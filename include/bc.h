@@ -146,8 +146,12 @@ bc_status bc_scatter_blocks(const void *d_packed, const int32_t *d_idx, const in
  *   d_residual shaped and typed like out, or NULL; read only at active blocks.
  *   d_out      must not overlap d_in, d_w or d_residual (BC_ERR_ALIAS).
  * Sizes: out.n = in.n, out.h = (in.h + 2*pad - kh)/stride + 1 (same for w).
- * Supported: stride 1 or 2; kh = kw in {1, 3, 5, 7}; NHWC needs Cin % 8 == 0 or
- * kw*Cin <= 32 (the stem form), and Cout % 16 == 0.
+ * Supported (else BC_ERR_UNSUPPORTED with the reason in bc_last_error()): stride 1
+ * or 2; kh = kw in {1, 3, 5, 7}. NHWC (matrix cores): Cout % 64 == 0; Cin % 8 == 0,
+ * or Cin <= 4 with kw <= 7, or Cin < 8 with kw <= 3 (the stem form); input, output
+ * and weights each below 2 GiB; the block width must divide 64 or 128 and the block's
+ * halo must fit in LDS. NCHW (fp32): output blocks of at most 2048 pixels whose halo
+ * tile (one channel) fits in LDS.
  * If d_out is a registered buffer (bc_buffer_register) that is not valid, a sparse
  * call (d_idx non-NULL) returns BC_ERR_UNINITIALIZED; a full call (d_idx = d_count
  * = NULL) makes it valid.
