@@ -975,8 +975,10 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 // and K split over every ResNet-50 layer of a 2048x1024 frame with 30 % of the blocks
 // active: 64-row tiles are fastest everywhere (at these sizes the kernel is bound by
 // latency and occupancy, and 64x64 tiles keep the most workgroups resident); 128-wide N
-// tiles pay off only for 1x1 layers with 64 input channels; splitting K pays off only
-// when a full frame has at most 256 tiles (the stride-32 layers), and then by 2.
+// tiles pay off only for 1x1 layers with 64 input channels; splitting K in two pays off
+// when a full frame has at most 256 tiles (the stride-32 layers) and for 3x3 layers
+// with 512 or more input channels and 513 to 2048 tiles (where nine-tap stages do not
+// apply).
 // Other forms take the largest tile with >= 2048 workgroups on a full frame. The choice
 // depends on the layer's shape only, never on the active count, so an active block's
 // result does not depend on which other blocks are active.
@@ -988,8 +990,12 @@ bool choose_plan(const LayerGeom &g, Plan &best)
             MfmaArgs &a = best.a;
             const int nchunk = (g.cin + BK - 1) / BK;
             const unsigned tiles = best.grid;
-            if (best.BM == 64 && best.BN == 64 && tiles <= 256 && nchunk >= 8 &&
-                tiles <= (unsigned)kMaxSplitTiles) {
+            // split K in two for few tiles with a long K, and for 3x3 layers with at least
+            // 512 input channels (sixteen chunks of nine taps per tile otherwise) whose
+            // tiles are too many for nine-tap stages
+            const bool split = (tiles <= 256 && nchunk >= 8) ||
+                               (g.kh == 3 && nchunk >= 16 && tiles > 512 && tiles <= 2048);
+            if (best.BM == 64 && best.BN == 64 && split && tiles <= (unsigned)kMaxSplitTiles) {
                 a.cps = (nchunk + 1) / 2;
                 a.ksplit = (nchunk + a.cps - 1) / a.cps;
                 best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
