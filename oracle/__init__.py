@@ -236,6 +236,43 @@ def sparse_maxpool2d(x_bits, mask, prev_bits, dtype, k=3, stride=2, pad=1):
     return select(mask, fresh, prev_bits, z.shape[2] // gh, z.shape[3] // gw)
 
 
+def upsample2x_bilinear(x):
+    """Bilinear upsampling by two of [n, c, h, w] values (float64), the sampling used by
+    SwiftNet-style decoders (pixel centres aligned, borders replicated): output row Y
+    samples input row (Y + 1/2) / 2 - 1/2, clamped to [0, h - 1], interpolated linearly
+    between its two neighbours; the same for columns. For a factor of two this gives
+    out[2i] = 3/4 in[i] + 1/4 in[i-1] and out[2i+1] = 3/4 in[i] + 1/4 in[i+1], with an
+    index outside the image replaced by the nearest edge row or column."""
+    x = np.asarray(x, np.float64)
+
+    def axis_up(a, axis):
+        n = a.shape[axis]
+        src = (np.arange(2 * n) + 0.5) / 2.0 - 0.5
+        src = np.clip(src, 0.0, n - 1)
+        lo = np.floor(src).astype(np.int64)
+        hi = np.minimum(lo + 1, n - 1)
+        f = src - lo
+        shape = [1] * a.ndim
+        shape[axis] = 2 * n
+        f = f.reshape(shape)
+        return np.take(a, lo, axis=axis) * (1.0 - f) + np.take(a, hi, axis=axis) * f
+
+    return axis_up(axis_up(x, 2), 3)
+
+
+def sparse_upsample_add(coarse_bits, skip_bits, mask, prev_bits, dtype, relu=False):
+    """One block-sparse decoder merge: up2(coarse) (+ skip) (ReLU), rounded to dtype,
+    selected into the previous output by the mask (the grid indexes output blocks)."""
+    z = upsample2x_bilinear(value(coarse_bits, dtype))
+    if skip_bits is not None:
+        z = z + value(skip_bits, dtype)
+    if relu:
+        z = np.maximum(z, 0.0)
+    fresh = store(z, dtype)
+    gh, gw = np.asarray(mask).shape[1:]
+    return select(mask, fresh, prev_bits, z.shape[2] // gh, z.shape[3] // gw)
+
+
 def gather_halo(x_bits, idx, gh, gw, bh, bw, kh, kw, stride, pad, pad_bits):
     """Halo tiles of the listed output blocks, packed [K, th, tw, C] (channels last):
     packed[k, i, j, c] = X[n, c, gy*bh*s - pad + i, gx*bw*s - pad + j], with

@@ -19,7 +19,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import fold_bn, sparse_conv2d, sparse_maxpool2d, store
+from . import fold_bn, sparse_conv2d, sparse_maxpool2d, sparse_upsample_add, store
 
 
 def resnet_table(depth: int):
@@ -64,6 +64,40 @@ def resnet_table(depth: int):
     return L
 
 
+def swiftnet_table(depth: int = 18, classes: int = 19, width: int = 128):
+    """A SwiftNet-like single-scale segmentation network (Orsic et al., 2019; the
+    paper's semantic segmentation model, Section 4): the ResNet encoder above, then a
+    decoder that runs at strides 32 -> 16 -> 8 -> 4. Each merge upsamples the coarser
+    decoder feature by two (bilinear) and adds a 1x1 lateral projection of the encoder
+    feature of the finer stride, then blends with a 3x3 convolution; a 1x1 head gives
+    the class scores at stride 4. Reading: the pyramid pooling on the stride-32
+    feature pools over the whole image, not per block, and is replaced by a 1x1
+    projection; the head computes a multiple of 64 channels (what the matrix-core
+    layers take) of which the first `classes` are the class scores. New layer kind
+    'up': src = coarse feature, res = lateral (skip)."""
+    L = resnet_table(depth)
+    ends = {}
+    for i, l in enumerate(L):
+        if l["name"].startswith("layer") and (i + 1 == len(L) or L[i + 1]["name"].split(".")[0] != l["name"].split(".")[0]):
+            ends[int(l["name"][5])] = i          # last layer of stage 1..4
+    expansion = 4 if depth == 50 else 1
+
+    def conv(name, src, cin, cout, k, relu):
+        L.append(dict(kind="conv", name=name, src=src, res=None, cin=cin, cout=cout,
+                      k=k, stride=1, pad=k // 2, relu=relu))
+        return len(L) - 1
+
+    x = conv("dec.proj4", ends[4], 512 * expansion, width, 1, True)
+    for s in (3, 2, 1):
+        lat = conv(f"dec.lat{s}", ends[s], (64 << (s - 1)) * expansion, width, 1, True)
+        L.append(dict(kind="up", name=f"dec.up{s}", src=x, res=lat, cin=width, cout=width,
+                      k=1, stride=1, pad=0, relu=False))
+        x = conv(f"dec.blend{s}", len(L) - 1, width, width, 3, True)
+    head = conv("dec.logits", x, width, -(-classes // 64) * 64, 1, False)
+    L[head]["classes"] = classes      # the first `classes` channels are the class scores
+    return L
+
+
 def make_params(table, seed0=1000, bn_random=False):
     """Per-conv fp32 OIHW weights (He-normal, seed seed0 + layer index) and BN
     parameters. Random init uses gamma=1, beta=0, mean=0, var=1 unless bn_random."""
@@ -103,6 +137,9 @@ def shapes(table, h, w):
     out = []
     for l in table:
         ih, iw = (h, w) if l["src"] < 0 else out[l["src"]][1:]
+        if l["kind"] == "up":
+            out.append((l["cout"], 2 * ih, 2 * iw))
+            continue
         oh = (ih + 2 * l["pad"] - l["k"]) // l["stride"] + 1
         ow = (iw + 2 * l["pad"] - l["k"]) // l["stride"] + 1
         out.append((l["cout"], oh, ow))
@@ -120,6 +157,8 @@ def frame(table, folded, x_bits, mask, prev, dtype):
         src = x_bits if l["src"] < 0 else bufs[l["src"]]
         if l["kind"] == "pool":
             y = sparse_maxpool2d(src, mask, prev[li], dtype, l["k"], l["stride"], l["pad"])
+        elif l["kind"] == "up":
+            y = sparse_upsample_add(src, bufs[l["res"]], mask, prev[li], dtype, relu=l["relu"])
         else:
             res = None if l["res"] is None else bufs[l["res"]]
             y = sparse_conv2d(src, folded[li]["w_bits"], mask, prev[li], dtype,
