@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 2
+#define BC_ABI_VERSION 3
 
 typedef enum {
     BC_OK = 0,
@@ -175,6 +175,31 @@ bc_status bc_sparse_maxpool2d(const bc_conv *geom, const void *d_in, bc_tensor i
                               void *stream);
 
 /*
+ * Block-sparse decoder merge (Section 4: the semantic segmentation network is a
+ * SwiftNet-style encoder-decoder, whose decoder upsamples a coarse feature map and adds
+ * the lateral features of the finer level):
+ *   out[block] = act(up2(coarse)[block] (+ skip[block]))  for the active blocks,
+ *   out[other] untouched (feature transfer).
+ * up2 is bilinear upsampling by two with pixel centres aligned and edges replicated:
+ * output row 2i takes 3/4 of coarse row i and 1/4 of row i-1, row 2i+1 takes 3/4 of
+ * row i and 1/4 of row i+1 (a row outside the image is replaced by the nearest edge
+ * row); columns alike. An output block reads a one-pixel coarse halo from d_coarse as
+ * it stands. act is ReLU when relu = 1. Arithmetic fp32, one round-to-nearest-even
+ * to out.dtype.
+ *   coarse, out  same dtype and layout; out = [n][c][2 coarse.h][2 coarse.w]. NHWC:
+ *                BF16 or F16 with c % 8 == 0, out below 2 GiB. NCHW: F32.
+ *   d_skip       shaped and typed like out, or NULL; read only at active blocks.
+ *   d_out        must not overlap d_coarse, d_skip or the index (BC_ERR_ALIAS).
+ * Index, capacity and registered-buffer rules as bc_sparse_conv2d.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE,
+ * BC_ERR_CAPACITY, BC_ERR_ALIAS, BC_ERR_UNINITIALIZED, BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ */
+bc_status bc_sparse_upsample_add(const void *d_coarse, bc_tensor coarse, const void *d_skip,
+                                 void *d_out, bc_tensor out, bc_grid g, int32_t relu,
+                                 const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                 void *stream);
+
+/*
  * Host only. Fold inference-mode batch normalisation into the preceding conv:
  * w_out = w * gamma / sqrt(var + eps), b_out = beta + (conv_bias - mean) * gamma /
  * sqrt(var + eps), computed in double and rounded to float. w is [cout][per_out]
@@ -264,15 +289,24 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
  * maximum over its pixels (Eq. 1):
  *   d_ig[n][gy][gx] = max over pixels p of block (gy, gx) of
  *                     sum_c O_t[c,p] (log O_t[c,p] - log O_{t-1}[c,p]).
- * Arithmetic: fp32 (log-sum-exp with the per-pixel maximum subtracted); a per-pixel
- * value below zero (rounding, the exact KL is >= 0) counts as 0.
- *   d_logits, d_prev_logits  float32 [n][c][h][w] (desc: F32, NCHW, 1 <= c <= 32).
+ * The class scores are the first `classes` channels of the score maps (the rest, e.g.
+ * channels a head pads to a tile multiple, is never read). The maps can be the
+ * network's output at any resolution (the blocks are desc.h / grid_h x desc.w / grid_w
+ * pixels of it). Arithmetic: fp32 (log-sum-exp with the per-pixel maximum subtracted);
+ * a per-pixel value below zero (rounding, the exact KL is >= 0) counts as 0. A block
+ * whose scores were copied from frame t-1 (not executed) gets exactly 0.
+ *   d_logits, d_prev_logits  frame t and frame t-1, same desc: F32 NCHW
+ *            [n][c][h][w], or BF16/F16 NHWC [n][h][w][c] with c % 8 == 0.
+ *   classes  1 .. min(c, 32).
  *   d_ig     float32 [n][grid_h][grid_w], device (written completely).
- * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE,
- * BC_ERR_ALIAS (d_ig overlapping an input), BC_ERR_UNSUPPORTED (c > 32), BC_ERR_HIP.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE (classes), BC_ERR_DTYPE (NCHW not F32, NHWC F32),
+ * BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE, BC_ERR_ALIAS (d_ig overlapping an input),
+ * BC_ERR_UNSUPPORTED (classes > 32, NHWC c % 8 != 0, an image's scores >= 2 GiB),
+ * BC_ERR_HIP.
  */
-bc_status bc_seg_information_gain(const float *d_logits, const float *d_prev_logits,
-                                  bc_tensor desc, bc_grid g, float *d_ig, void *stream);
+bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logits,
+                                  bc_tensor desc, int32_t classes, bc_grid g, float *d_ig,
+                                  void *stream);
 
 /*
  * Block rewards and the policy loss (Section 3.5), per image n of the batch:

@@ -71,7 +71,9 @@ _sigs = {
     "bc_sample_execution_grid": ([_vp, _i32, bc_grid, ctypes.c_uint64, ctypes.c_uint64, _vp, _vp, _i32,
                                   _vp, _vp, _vp], _i32),
     "bc_update_frame_state": ([_vp, _vp, bc_tensor, bc_grid, _vp, _vp, _i32, _vp], _i32),
-    "bc_seg_information_gain": ([_vp, _vp, bc_tensor, bc_grid, _vp, _vp], _i32),
+    "bc_sparse_upsample_add": ([_vp, bc_tensor, _vp, _vp, bc_tensor, bc_grid, _i32, _vp, _vp, _i32,
+                                _vp], _i32),
+    "bc_seg_information_gain": ([_vp, _vp, bc_tensor, _i32, bc_grid, _vp, _vp], _i32),
     "bc_block_rewards": ([_vp, _vp, _vp, _i32, bc_grid, _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
@@ -80,6 +82,13 @@ for _name, (_args, _res) in _sigs.items():
     _fn.restype = _res
 
 EXPORTED = tuple(_sigs)
+
+# The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
+# from other sources is refused rather than called with mismatched arguments.
+ABI_VERSION = 3
+if _lib.bc_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
+                      f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
 
 
 def status_name(s: int) -> str:
@@ -194,6 +203,20 @@ def bc_sparse_maxpool2d(geom, x, layout, out, grid, idx, count, stream=None):
     _check(st, "bc_sparse_maxpool2d")
 
 
+def bc_sparse_upsample_add(coarse, layout, skip, out, grid, relu, idx, count, stream=None):
+    """out[active blocks] = relu?(up2(coarse) + skip); out is [n, c, 2h, 2w] of coarse
+    (NHWC or NCHW order per layout), skip shaped like out or None."""
+    cap = 0 if idx is None else int(idx.numel())
+    if skip is not None and (skip.shape != out.shape or skip.dtype != out.dtype):
+        raise ValueError("skip must be shaped and typed like out")
+    if skip is not None and not skip.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    st = _lib.bc_sparse_upsample_add(_ptr(coarse), desc(coarse, layout), _ptr(skip), _ptr(out),
+                                     desc(out, layout), _grid(grid), int(relu), _ptr(idx),
+                                     _ptr(count), cap, _stream(stream))
+    _check(st, "bc_sparse_upsample_add")
+
+
 def bc_sample_execution_grid(prob, grid, seed, frame, mask, idx, count, h_count=None, stream=None):
     """prob float32 [n, gh, gw] (device) -> mask uint8 [n, gh, gw], idx int32 [capacity],
     count int32 [1] (device). With h_count=True the count is also returned (synchronising)."""
@@ -216,12 +239,17 @@ def bc_update_frame_state(frame, state, layout, grid, idx, count, stream=None):
     _check(st, "bc_update_frame_state")
 
 
-def bc_seg_information_gain(logits, prev_logits, grid, ig, stream=None):
-    """logits, prev_logits float32 [n, classes, h, w] -> ig float32 [n, gh, gw]."""
-    if logits.shape != prev_logits.shape:
-        raise ValueError("score maps must have the same shape")
-    st = _lib.bc_seg_information_gain(_ptr(logits), _ptr(prev_logits), desc(logits, BC_NCHW),
-                                      _grid(grid), _ptr(ig), _stream(stream))
+def bc_seg_information_gain(logits, prev_logits, grid, ig, classes=None, layout=BC_NCHW,
+                            stream=None):
+    """Score maps of frames t and t-1 (float32 [n, c, h, w], or bf16/f16 [n, h, w, c] with
+    layout=BC_NHWC) -> ig float32 [n, gh, gw]; the first `classes` channels (default all)
+    are the class scores."""
+    if logits.shape != prev_logits.shape or logits.dtype != prev_logits.dtype:
+        raise ValueError("score maps must have the same shape and dtype")
+    d = desc(logits, layout)
+    st = _lib.bc_seg_information_gain(_ptr(logits), _ptr(prev_logits), d,
+                                      int(d.c if classes is None else classes), _grid(grid),
+                                      _ptr(ig), _stream(stream))
     _check(st, "bc_seg_information_gain")
 
 

@@ -553,26 +553,80 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
     return ok();
 }
 
-bc_status bc_seg_information_gain(const float *d_logits, const float *d_prev_logits,
-                                  bc_tensor desc, bc_grid g, float *d_ig, void *stream)
+bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logits,
+                                  bc_tensor desc, int32_t classes, bc_grid g, float *d_ig,
+                                  void *stream)
 {
     if (!d_logits || !d_prev_logits || !d_ig)
         return fail(BC_ERR_NULL, "d_logits, d_prev_logits and d_ig are required");
     bc_status st = check_tensor(desc, "desc");
     if (st) return st;
-    if (desc.dtype != BC_F32) return fail(BC_ERR_DTYPE, "scores must be float32");
-    if (desc.layout != BC_NCHW) return fail(BC_ERR_LAYOUT, "scores must be NCHW ([n][classes][h][w])");
+    if (desc.layout == BC_NCHW && desc.dtype != BC_F32)
+        return fail(BC_ERR_DTYPE, "channels-first scores must be float32");
+    if (desc.layout == BC_NHWC && desc.dtype == BC_F32)
+        return fail(BC_ERR_DTYPE, "channels-last scores must be bf16 or f16");
+    if (desc.layout == BC_NHWC && desc.c % 8)
+        return fail(BC_ERR_UNSUPPORTED, "channels-last scores need C %% 8 == 0 (got %d)", desc.c);
+    if (classes < 1 || classes > desc.c)
+        return fail(BC_ERR_SHAPE, "classes %d outside 1..%d (the channel count)", classes, desc.c);
+    if (classes > 32) return fail(BC_ERR_UNSUPPORTED, "at most 32 classes (got %d)", classes);
     LayerGeom L;
     if ((st = block_geom(desc, g, L))) return st;
-    if (desc.c > 32) return fail(BC_ERR_UNSUPPORTED, "at most 32 classes (got %d)", desc.c);
-    const double img_bytes = 4.0 * desc.c * desc.h * desc.w;
+    const int es = esize_of(desc.dtype);
+    const double img_bytes = (double)es * desc.c * desc.h * desc.w;
     if (img_bytes >= 2147483392.0) return fail(BC_ERR_UNSUPPORTED, "one image's scores must be < 2 GiB");
     const size_t bytes = tensor_bytes(desc), igb = (size_t)L.total_blocks * 4;
     if (overlap(d_ig, igb, d_logits, bytes) || overlap(d_ig, igb, d_prev_logits, bytes))
         return fail(BC_ERR_ALIAS, "d_ig overlaps an input");
-    hipError_t e = bc::launch_seg_information_gain(d_logits, d_prev_logits, desc.n, desc.c, desc.h,
-                                                   desc.w, g.grid_h, g.grid_w, d_ig, (hipStream_t)stream);
+    hipError_t e = bc::launch_seg_information_gain(
+        d_logits, d_prev_logits, desc.n, desc.c, classes, desc.h, desc.w, es,
+        desc.layout == BC_NHWC, desc.dtype == BC_BF16, g.grid_h, g.grid_w, d_ig,
+        (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "information gain launch");
+    return ok();
+}
+
+bc_status bc_sparse_upsample_add(const void *d_coarse, bc_tensor coarse, const void *d_skip,
+                                 void *d_out, bc_tensor out, bc_grid g, int32_t relu,
+                                 const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                 void *stream)
+{
+    if (!d_coarse || !d_out) return fail(BC_ERR_NULL, "d_coarse and d_out are required");
+    bc_status st;
+    if ((st = check_tensor(coarse, "coarse"))) return st;
+    if ((st = check_tensor(out, "out"))) return st;
+    if (coarse.dtype != out.dtype) return fail(BC_ERR_DTYPE, "coarse and out dtypes differ");
+    if (coarse.layout != out.layout) return fail(BC_ERR_LAYOUT, "coarse and out layouts differ");
+    if (out.layout == BC_NHWC && out.dtype == BC_F32)
+        return fail(BC_ERR_UNSUPPORTED, "channels-last maps take BF16 or F16");
+    if (out.layout == BC_NCHW && out.dtype != BC_F32)
+        return fail(BC_ERR_UNSUPPORTED, "channels-first maps take F32");
+    if (out.layout == BC_NHWC && out.c % 8)
+        return fail(BC_ERR_UNSUPPORTED, "channels-last maps need C %% 8 == 0 (got %d)", out.c);
+    if (out.n != coarse.n || out.c != coarse.c || out.h != 2 * coarse.h || out.w != 2 * coarse.w)
+        return fail(BC_ERR_SHAPE, "out must be [n][c][2h][2w] of coarse's [n][c][h][w]");
+    if (relu != 0 && relu != 1) return fail(BC_ERR_SHAPE, "relu must be 0 or 1");
+    LayerGeom L;
+    if ((st = block_geom(out, g, L))) return st;
+    if ((st = check_index(d_idx, d_count, capacity, L.total_blocks))) return st;
+    const size_t ob = tensor_bytes(out), cb = tensor_bytes(coarse);
+    if (out.layout == BC_NHWC) {
+        if (ob >= 2147483392u) return fail(BC_ERR_UNSUPPORTED, "channels-last out must be < 2 GiB");
+        const double chunks = ceil((double)L.bh * L.bw * (out.c / 8) / 256.0);
+        if (chunks * L.total_blocks >= 4194304.0)
+            return fail(BC_ERR_UNSUPPORTED, "too many workgroups (blocks x block size)");
+    }
+    if (overlap(d_out, ob, d_coarse, cb)) return fail(BC_ERR_ALIAS, "d_out overlaps d_coarse");
+    if (overlap(d_out, ob, d_skip, ob)) return fail(BC_ERR_ALIAS, "d_out overlaps d_skip");
+    if (d_idx && (overlap(d_out, ob, d_idx, (size_t)capacity * 4) || overlap(d_out, ob, d_count, 4)))
+        return fail(BC_ERR_ALIAS, "d_out overlaps the index");
+    if ((st = check_registered(d_out, out, d_idx != nullptr))) return st;
+    hipError_t e = bc::launch_upsample_add(d_coarse, d_skip, d_out, out.n, out.c, coarse.h,
+                                           coarse.w, esize_of(out.dtype), out.layout == BC_NHWC,
+                                           out.dtype == BC_BF16, g.grid_h, g.grid_w, d_idx,
+                                           d_count, relu, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "upsample launch");
+    if (!d_idx) mark_full(d_out);
     return ok();
 }
 

@@ -54,12 +54,20 @@ hipError_t launch_sample_index(const float *prob, int total, uint64_t seed, uint
 hipError_t launch_frame_state(const void *frame, void *state, int n, int c, int h, int w,
                               int esize, bool nhwc, int gh, int gw, const int32_t *idx,
                               const int32_t *count, hipStream_t s);
-// Per-block maximum of the per-pixel KL divergence of two [n][c][h][w] score maps.
-hipError_t launch_seg_information_gain(const float *lt, const float *lp, int n, int c, int h,
-                                       int w, int gh, int gw, float *ig, hipStream_t s);
+// Per-block maximum of the per-pixel KL divergence of two score maps: the first
+// `classes` of c channels, [n][c][h][w] fp32 or [n][h][w][c] bf16/fp16 (c % 8 == 0).
+hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, int c, int classes,
+                                       int h, int w, int esize, bool nhwc, bool bf16, int gh,
+                                       int gw, float *ig, hipStream_t s);
 // Rewards, cost, moving average and REINFORCE loss per image.
 hipError_t launch_block_rewards(const float *ig, const uint8_t *mask, const float *prob, int n,
                                 int blocks, float tau, float gamma, float mu, float *mavg,
                                 float *reward, float *cost, float *loss, hipStream_t s);
+
+// Decoder merge: out = up2(coarse) (+ skip) (ReLU) on the active output blocks; coarse
+// [n][hc][wc][c] (bf16/fp16, c % 8 == 0) or [n][c][hc][wc] fp32, out/skip 2hc x 2wc.
+hipError_t launch_upsample_add(const void *coarse, const void *skip, void *out, int n, int c,
+                               int hc, int wc, int esize, bool nhwc, bool bf16, int gh, int gw,
+                               const int32_t *idx, const int32_t *count, int relu, hipStream_t s);
 
 }  // namespace bc

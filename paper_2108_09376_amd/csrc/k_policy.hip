@@ -88,6 +88,7 @@ constexpr int kCopyVecPerThread = 4;
 constexpr int kCopyVecPerWG = kCopyThreads * kCopyVecPerThread;
 constexpr int kBufferFlags = 0x00020000;     // raw buffer, dword format
 constexpr int kOutOfRange = 0x7FFFFF00;      // loads return 0, stores are dropped
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 struct CopyGeom {
     int gh, gw, bh, bw, total_blocks;
@@ -193,67 +194,75 @@ __global__ void k_fill_zero(float *__restrict__ p, int n)
     if (i < n) p[i] = 0.f;
 }
 
-// One workgroup covers `rows` image rows of one block (about kIgPixPerWG pixels).
-// Per pixel: all 2*C scores are requested at once (raw buffer loads, classes past C
-// return zero and are masked out of every sum), then
-//   KL = sum_c e^(l_c - Ml) (l_c - m_c) / Sl - (Ml + log Sl) + (Mm + log Sm),
-// Ml, Mm = per-pixel maxima, Sl, Sm = sums of e^(x - max): that is
-// sum_c p_c (log p_c - log q_c) with p = softmax(l), q = softmax(m). The workgroup's
-// maximum goes to the block's slot with an integer atomic max (the values are >= 0,
-// whose IEEE bit patterns order like the numbers; the slot starts at +0).
-template <int CMAX>
-__global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
-    const float *__restrict__ lt, const float *__restrict__ lp, int C, int h, int w, int gh,
-    int gw, int rows, int strips, int bytes, float *__restrict__ ig)
+template <bool BF16>
+__device__ __forceinline__ float h16_to_f32(uint32_t h)
 {
-    __shared__ float wave_max[kIgThreads / 64];
-    const int blk = blockIdx.x / strips;
-    const int strip = blockIdx.x - blk * strips;
-    const int img = blk / (gh * gw);
-    const int rem = blk - img * gh * gw;
-    const int gy = rem / gw, gx = rem - gy * gw;
-    const int bh = h / gh, bw = w / gw;
-    const int y0 = gy * bh + strip * rows;
-    const int nrows = min(rows, gy * bh + bh - y0);
-    const int npix = nrows * bw;
-    const size_t plane = (size_t)h * w;
-    const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(lt + (size_t)img * C * plane), (short)0, bytes, kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(lp + (size_t)img * C * plane), (short)0, bytes, kBufferFlags);
-    float best = 0.f;
-    for (int p = threadIdx.x; p < npix; p += kIgThreads) {
-        const int y = y0 + p / bw, x = gx * bw + p % bw;
-        const int pix = (y * w + x) * 4;
-        float a[CMAX], b[CMAX];
+    if constexpr (BF16) return __uint_as_float(h << 16);
+    else return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+// KL(p || q) of one pixel from its first C class scores a (frame t) and b (frame t-1),
+// p = softmax(a), q = softmax(b):
+//   sum_c e^(a_c - Ma) (a_c - b_c) / Sa - (Ma + log Sa) + (Mb + log Sb),
+// Ma, Mb = maxima, Sa, Sb = sums of e^(x - max). Entries past C are ignored.
+template <int CMAX>
+__device__ __forceinline__ float pixel_kl(const float (&a)[CMAX], const float (&b)[CMAX], int C)
+{
+    float ml = -__builtin_inff(), mm = -__builtin_inff();
 #pragma unroll
-        for (int c = 0; c < CMAX; ++c) {
-            const int o = c < C ? pix + c * (int)plane * 4 : kOutOfRange;
-            a[c] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rt, o, 0, 0));
-            b[c] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, o, 0, 0));
+    for (int c = 0; c < CMAX; ++c) {
+        if (c < C) {
+            ml = fmaxf(ml, a[c]);
+            mm = fmaxf(mm, b[c]);
         }
-        float ml = -__builtin_inff(), mm = -__builtin_inff();
-#pragma unroll
-        for (int c = 0; c < CMAX; ++c) {
-            if (c < C) {
-                ml = fmaxf(ml, a[c]);
-                mm = fmaxf(mm, b[c]);
-            }
-        }
-        float sl = 0.f, sm = 0.f, t = 0.f;
-#pragma unroll
-        for (int c = 0; c < CMAX; ++c) {
-            if (c < C) {
-                const float ea = __expf(a[c] - ml);
-                sl += ea;
-                t += ea * (a[c] - b[c]);
-                sm += __expf(b[c] - mm);
-            }
-        }
-        const float kl = t / sl - (ml + __logf(sl)) + (mm + __logf(sm));
-        best = kl > best ? kl : best;
     }
-    // workgroup maximum: within each wave by butterfly, then across the four waves
+    float sl = 0.f, sm = 0.f, t = 0.f;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+        if (c < C) {
+            const float ea = __expf(a[c] - ml);
+            sl += ea;
+            t += ea * (a[c] - b[c]);
+            sm += __expf(b[c] - mm);
+        }
+    }
+    return t / sl - (ml + __logf(sl)) + (mm + __logf(sm));
+}
+
+struct IgGeom {
+    int classes;       // class scores per pixel (the first `classes` channels)
+    int c;             // channels of the score tensor (>= classes)
+    int h, w, gh, gw;
+    int rows, strips;  // image rows per workgroup, workgroups per block
+    int bytes;         // one image's scores in bytes (< 2 GiB)
+};
+
+// Which block and which rows of it a workgroup covers.
+struct IgPart {
+    int blk, img, gx, y0, npix, bw;
+};
+
+__device__ __forceinline__ IgPart ig_part(const IgGeom &g)
+{
+    IgPart q;
+    q.blk = blockIdx.x / g.strips;
+    const int strip = blockIdx.x - q.blk * g.strips;
+    q.img = q.blk / (g.gh * g.gw);
+    const int rem = q.blk - q.img * g.gh * g.gw;
+    const int gy = rem / g.gw;
+    q.gx = rem - gy * g.gw;
+    const int bh = g.h / g.gh;
+    q.bw = g.w / g.gw;
+    q.y0 = gy * bh + strip * g.rows;
+    q.npix = min(g.rows, gy * bh + bh - q.y0) * q.bw;
+    return q;
+}
+
+// Workgroup maximum (butterfly within each wave, then across the waves) into the
+// block's slot by an integer atomic max: the values are >= 0, whose IEEE bit patterns
+// order like the numbers, and the slot starts at +0.
+__device__ __forceinline__ void block_max_out(float best, float *wave_max, float *slot)
+{
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o));
     if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = best;
@@ -262,8 +271,80 @@ __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
         float m = wave_max[0];
 #pragma unroll
         for (int i = 1; i < kIgThreads / 64; ++i) m = fmaxf(m, wave_max[i]);
-        atomicMax((unsigned int *)&ig[blk], __float_as_uint(m));
+        atomicMax((unsigned int *)slot, __float_as_uint(m));
     }
+}
+
+// Channels first, fp32: one workgroup covers `rows` image rows of one block (about
+// kIgPixPerWG pixels); per pixel all 2*classes scores are requested at once (raw buffer
+// loads, classes past the count return zero and are left out of every sum).
+template <int CMAX>
+__global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
+    const float *__restrict__ lt, const float *__restrict__ lp, IgGeom g, float *__restrict__ ig)
+{
+    __shared__ float wave_max[kIgThreads / 64];
+    const IgPart q = ig_part(g);
+    const size_t plane = (size_t)g.h * g.w;
+    const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(lt + (size_t)q.img * g.c * plane), (short)0, g.bytes, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(lp + (size_t)q.img * g.c * plane), (short)0, g.bytes, kBufferFlags);
+    float best = 0.f;
+    for (int p = threadIdx.x; p < q.npix; p += kIgThreads) {
+        const int y = q.y0 + p / q.bw, x = q.gx * q.bw + p % q.bw;
+        const int pix = (y * g.w + x) * 4;
+        float a[CMAX], b[CMAX];
+#pragma unroll
+        for (int c = 0; c < CMAX; ++c) {
+            const int o = c < g.classes ? pix + c * (int)plane * 4 : kOutOfRange;
+            a[c] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rt, o, 0, 0));
+            b[c] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, o, 0, 0));
+        }
+        const float kl = pixel_kl<CMAX>(a, b, g.classes);
+        best = kl > best ? kl : best;
+    }
+    block_max_out(best, wave_max, &ig[q.blk]);
+}
+
+// Channels last, bf16/fp16 (c % 8 == 0): per pixel the CV 16-byte vectors that hold the
+// class scores (8 channels each, CV = ceil(classes / 8)) of both maps are requested at
+// once; arithmetic in fp32 as above.
+template <bool BF16, int CV>
+__global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax_nhwc16(
+    const uint4 *__restrict__ lt, const uint4 *__restrict__ lp, IgGeom g, float *__restrict__ ig)
+{
+    __shared__ float wave_max[kIgThreads / 64];
+    const IgPart q = ig_part(g);
+    const int vpp = g.c / 8;
+    const size_t img_vec = (size_t)g.h * g.w * vpp;
+    const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(lt + q.img * img_vec), (short)0, g.bytes, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(lp + q.img * img_vec), (short)0, g.bytes, kBufferFlags);
+    float best = 0.f;
+    for (int p = threadIdx.x; p < q.npix; p += kIgThreads) {
+        const int y = q.y0 + p / q.bw, x = q.gx * q.bw + p % q.bw;
+        const int base = (y * g.w + x) * vpp * 16;
+        i32x4 va[CV], vb[CV];
+#pragma unroll
+        for (int j = 0; j < CV; ++j) {
+            va[j] = __builtin_amdgcn_raw_buffer_load_b128(rt, base + 16 * j, 0, 0);
+            vb[j] = __builtin_amdgcn_raw_buffer_load_b128(rp, base + 16 * j, 0, 0);
+        }
+        float a[8 * CV], b[8 * CV];
+#pragma unroll
+        for (int j = 0; j < CV; ++j) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int sh = 16 * (t & 1);
+                a[8 * j + t] = h16_to_f32<BF16>(((uint32_t)va[j][t >> 1] >> sh) & 0xFFFFu);
+                b[8 * j + t] = h16_to_f32<BF16>(((uint32_t)vb[j][t >> 1] >> sh) & 0xFFFFu);
+            }
+        }
+        const float kl = pixel_kl<8 * CV>(a, b, g.classes);
+        best = kl > best ? kl : best;
+    }
+    block_max_out(best, wave_max, &ig[q.blk]);
 }
 
 // ---------------------------------------------------------------- rewards
@@ -378,26 +459,44 @@ hipError_t launch_frame_state(const void *frame, void *state, int n, int c, int 
     return hipGetLastError();
 }
 
-hipError_t launch_seg_information_gain(const float *lt, const float *lp, int n, int c, int h,
-                                       int w, int gh, int gw, float *ig, hipStream_t s)
+template <bool BF16>
+static void launch_ig_nhwc16(const void *lt, const void *lp, const IgGeom &g, dim3 grid, float *ig,
+                      hipStream_t s)
+{
+    const uint4 *a = (const uint4 *)lt, *b = (const uint4 *)lp;
+    switch ((g.classes + 7) / 8) {
+    case 1: hipLaunchKernelGGL((k_seg_kl_blockmax_nhwc16<BF16, 1>), grid, dim3(kIgThreads), 0, s, a, b, g, ig); break;
+    case 2: hipLaunchKernelGGL((k_seg_kl_blockmax_nhwc16<BF16, 2>), grid, dim3(kIgThreads), 0, s, a, b, g, ig); break;
+    case 3: hipLaunchKernelGGL((k_seg_kl_blockmax_nhwc16<BF16, 3>), grid, dim3(kIgThreads), 0, s, a, b, g, ig); break;
+    default: hipLaunchKernelGGL((k_seg_kl_blockmax_nhwc16<BF16, 4>), grid, dim3(kIgThreads), 0, s, a, b, g, ig); break;
+    }
+}
+
+hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, int c, int classes,
+                                       int h, int w, int esize, bool nhwc, bool bf16, int gh,
+                                       int gw, float *ig, hipStream_t s)
 {
     const int blocks = n * gh * gw;
     hipLaunchKernelGGL(k_fill_zero, dim3((blocks + 255) / 256), dim3(256), 0, s, ig, blocks);
+    IgGeom g;
+    g.classes = classes; g.c = c; g.h = h; g.w = w; g.gh = gh; g.gw = gw;
     const int bh = h / gh, bw = w / gw;
-    int rows = kIgPixPerWG / bw;
-    rows = rows < 1 ? 1 : (rows > bh ? bh : rows);
-    const int strips = (bh + rows - 1) / rows;
-    const int bytes = (int)((size_t)c * h * w * 4);   // one image's scores (checked < 2 GiB)
-    const dim3 grid((unsigned)blocks * strips), block(kIgThreads);
-    if (c == 19)
-        hipLaunchKernelGGL(k_seg_kl_blockmax<19>, grid, block, 0, s, lt, lp, c, h, w, gh, gw,
-                           rows, strips, bytes, ig);
-    else if (c <= 8)
-        hipLaunchKernelGGL(k_seg_kl_blockmax<8>, grid, block, 0, s, lt, lp, c, h, w, gh, gw,
-                           rows, strips, bytes, ig);
-    else
-        hipLaunchKernelGGL(k_seg_kl_blockmax<32>, grid, block, 0, s, lt, lp, c, h, w, gh, gw,
-                           rows, strips, bytes, ig);
+    g.rows = kIgPixPerWG / bw;
+    g.rows = g.rows < 1 ? 1 : (g.rows > bh ? bh : g.rows);
+    g.strips = (bh + g.rows - 1) / g.rows;
+    g.bytes = (int)((size_t)c * h * w * esize);   // one image's scores (checked < 2 GiB)
+    const dim3 grid((unsigned)blocks * g.strips), block(kIgThreads);
+    const float *a = (const float *)lt, *b = (const float *)lp;
+    if (nhwc) {
+        if (bf16) launch_ig_nhwc16<true>(lt, lp, g, grid, ig, s);
+        else launch_ig_nhwc16<false>(lt, lp, g, grid, ig, s);
+    } else if (classes == 19) {
+        hipLaunchKernelGGL(k_seg_kl_blockmax<19>, grid, block, 0, s, a, b, g, ig);
+    } else if (classes <= 8) {
+        hipLaunchKernelGGL(k_seg_kl_blockmax<8>, grid, block, 0, s, a, b, g, ig);
+    } else {
+        hipLaunchKernelGGL(k_seg_kl_blockmax<32>, grid, block, 0, s, a, b, g, ig);
+    }
     return hipGetLastError();
 }
 

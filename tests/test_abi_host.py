@@ -29,7 +29,7 @@ def test_header_declares_the_boundary():
               "bc_sparse_maxpool2d", "bc_fold_bn", "bc_buffer_register", "bc_buffer_release",
               "bc_buffer_invalidate", "bc_buffer_mark_written", "bc_buffer_is_valid",
               "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
-              "bc_block_rewards"]:
+              "bc_block_rewards", "bc_sparse_upsample_add"]:
         assert n in names
 
 
@@ -38,7 +38,8 @@ def test_library_exports_every_declared_symbol(B):
     for n in declared_functions():
         assert hasattr(lib, n), n
     assert set(B.EXPORTED) == set(declared_functions())
-    assert B.bc_abi_version() == 2
+    hdr = open(os.path.join(ROOT, "include", "bc.h")).read()
+    assert B.bc_abi_version() == B.ABI_VERSION == int(re.search(r"#define BC_ABI_VERSION (\d+)", hdr).group(1))
     # and the symbols are plain C (unmangled)
     out = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
     for n in declared_functions():
@@ -160,14 +161,36 @@ def test_policy_step_validation_codes(B):
     assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, d, g, FAKE_IDX, FAKE_CNT, 100, None) == B.BC_ERR_CAPACITY
     assert lib.bc_update_frame_state(FAKE_IN, FAKE_IN + 1024, d, g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_ALIAS
     assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, B.bc_tensor(1, 3, 1024, 2048, 7, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_DTYPE
-    # information gain
+    # information gain: fp32 channels first or 16-bit channels last; `classes` leading channels
     sc = B.bc_tensor(1, 19, 1024, 2048, 0, 0)
-    assert lib.bc_seg_information_gain(FAKE_IN, None, sc, g, FAKE_OUT, None) == B.BC_ERR_NULL
-    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 19, 1024, 2048, 1, 0), g, FAKE_OUT, None) == B.BC_ERR_DTYPE
-    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 19, 1024, 2048, 0, 1), g, FAKE_OUT, None) == B.BC_ERR_LAYOUT
-    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, B.bc_tensor(1, 33, 1024, 2048, 0, 0), g, FAKE_OUT, None) == B.BC_ERR_UNSUPPORTED
-    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, sc, B.bc_grid(3, 16), FAKE_OUT, None) == B.BC_ERR_NOT_DIVISIBLE
-    assert lib.bc_seg_information_gain(FAKE_IN, FAKE_W, sc, g, FAKE_W + 64, None) == B.BC_ERR_ALIAS
+    ig = lambda d, cls=19, gg=g, out=FAKE_OUT, a=FAKE_IN, b=FAKE_W: lib.bc_seg_information_gain(a, b, d, cls, gg, out, None)
+    assert ig(sc, b=None) == B.BC_ERR_NULL
+    assert ig(B.bc_tensor(1, 19, 1024, 2048, 1, 0)) == B.BC_ERR_DTYPE        # bf16 channels first
+    assert ig(B.bc_tensor(1, 24, 256, 512, 0, 1), 19) == B.BC_ERR_DTYPE      # f32 channels last
+    assert ig(B.bc_tensor(1, 19, 1024, 2048, 0, 5)) == B.BC_ERR_LAYOUT
+    assert ig(B.bc_tensor(1, 33, 1024, 2048, 0, 0), 33) == B.BC_ERR_UNSUPPORTED
+    assert ig(B.bc_tensor(1, 20, 256, 512, 1, 1), 19) == B.BC_ERR_UNSUPPORTED   # C % 8 != 0
+    assert ig(sc, 0) == B.BC_ERR_SHAPE and ig(sc, 20) == B.BC_ERR_SHAPE
+    assert ig(sc, gg=B.bc_grid(3, 16)) == B.BC_ERR_NOT_DIVISIBLE
+    assert ig(sc, out=FAKE_W + 64) == B.BC_ERR_ALIAS
+    # decoder merge: out = up2(coarse) (+ skip) on active blocks
+    cs, os_ = B.bc_tensor(1, 128, 128, 256, 1, 1), B.bc_tensor(1, 128, 256, 512, 1, 1)
+    up = lambda c=cs, o=os_, coarse=FAKE_IN, skip=FAKE_RES, out=FAKE_OUT, gg=g, relu=0, idx=FAKE_IDX, cnt=FAKE_CNT, cap=128: \
+        lib.bc_sparse_upsample_add(coarse, c, skip, out, o, gg, relu, idx, cnt, cap, None)
+    assert up(coarse=None) == B.BC_ERR_NULL and up(out=None) == B.BC_ERR_NULL
+    assert up(cnt=None) == B.BC_ERR_NULL
+    assert up(o=B.bc_tensor(1, 128, 256, 512, 2, 1)) == B.BC_ERR_DTYPE
+    assert up(o=B.bc_tensor(1, 128, 256, 512, 1, 0)) == B.BC_ERR_LAYOUT
+    assert up(o=B.bc_tensor(1, 128, 256, 510, 1, 1)) == B.BC_ERR_SHAPE     # not 2x coarse
+    assert up(o=B.bc_tensor(1, 64, 256, 512, 1, 1)) == B.BC_ERR_SHAPE      # channels differ
+    assert up(c=B.bc_tensor(1, 12, 128, 256, 1, 1), o=B.bc_tensor(1, 12, 256, 512, 1, 1)) == B.BC_ERR_UNSUPPORTED
+    assert up(c=B.bc_tensor(1, 16, 128, 256, 0, 1), o=B.bc_tensor(1, 16, 256, 512, 0, 1)) == B.BC_ERR_UNSUPPORTED
+    assert up(c=B.bc_tensor(1, 16, 128, 256, 1, 0), o=B.bc_tensor(1, 16, 256, 512, 1, 0)) == B.BC_ERR_UNSUPPORTED
+    assert up(relu=2) == B.BC_ERR_SHAPE
+    assert up(gg=B.bc_grid(3, 16)) == B.BC_ERR_NOT_DIVISIBLE
+    assert up(cap=127) == B.BC_ERR_CAPACITY
+    assert up(out=FAKE_IN + 4096) == B.BC_ERR_ALIAS and up(skip=FAKE_OUT + 16) == B.BC_ERR_ALIAS
+    assert up(idx=FAKE_OUT + 64) == B.BC_ERR_ALIAS
     # rewards
     f = ctypes.c_float
     args = lambda **kw: [kw.get(k, v) for k, v in [("ig", FAKE_IN), ("mask", FAKE_W), ("prob", FAKE_RES), ("n", 1), ("g", g),
@@ -196,6 +219,9 @@ def test_buffer_registry_rules(B):
     # a descriptor that differs from the registered one is refused (here: F16 vs BF16)
     assert conv_call(B, d_out=FAKE_OUT, inp=(1, 64, 64, 128, 2, 1),
                      out=(1, 64, 64, 128, 2, 1))[0] == B.BC_ERR_SHAPE
+    up = lambda idx: lib.bc_sparse_upsample_add(FAKE_IN, B.bc_tensor(1, 64, 32, 64, 1, 1), None, FAKE_OUT, desc,
+                                                 B.bc_grid(8, 16), 0, idx, idx and FAKE_CNT, 128, None)
+    assert up(FAKE_IDX) == B.BC_ERR_UNINITIALIZED
     assert lib.bc_buffer_mark_written(h, 0) == B.BC_ERR_UNINITIALIZED
     assert lib.bc_buffer_mark_written(h, 1) == B.BC_OK and lib.bc_buffer_is_valid(h) == 1
     assert lib.bc_buffer_mark_written(h, 0) == B.BC_OK

@@ -1,0 +1,168 @@
+"""GPU parity of the decoder-side steps of the segmentation network (Section 4, the
+SwiftNet-style decoder; Section 3.4, information gain) through the C ABI against the
+oracle on the same seeded inputs:
+
+* block-sparse upsample-and-add: copied blocks bit for bit, executed blocks within
+  max abs-rel 2e-2 (bf16, fp16) / 1e-4 (fp32) of the fp64 oracle, rounded once;
+* information gain on channels-last 16-bit score maps whose first `classes` channels
+  are the class scores (the rest padding that must never be read): within 1e-4 of the
+  fp64 oracle on the same decoded values."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from oracle import policy as P
+from tests._util import TOL, block_select, from_dev, max_abs_rel, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B(gpu):
+    from paper_2108_09376_amd import bc
+    return bc
+
+
+def _index(B, mask_np):
+    n, gh, gw = mask_np.shape
+    m = torch.from_numpy(mask_np).cuda()
+    idx = torch.full((n * gh * gw + 3,), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    B.bc_build_block_index(m, n, (gh, gw), idx, cnt)
+    return idx, cnt
+
+
+def _check_merge(got, want, mask, dtype):
+    sel = block_select(mask, want.shape)
+    assert np.array_equal(got[~sel], want[~sel]), "copied blocks changed"
+    g, w = oracle.value(got[sel], dtype), oracle.value(want[sel], dtype)
+    assert max_abs_rel(g, w) <= TOL[dtype]
+
+
+# ------------------------------------------------------------------ upsample + add
+
+@pytest.mark.parametrize("dtype,nhwc,n,c,hc,wc,grid,p,skip,relu", [
+    ("bf16", True, 1, 128, 32, 64, (8, 16), 0.3, True, False),    # 8x8-pixel blocks
+    ("bf16", True, 2, 24, 20, 28, (4, 7), 0.5, True, True),       # 10x8 blocks, 3 vectors/px
+    ("f16", True, 1, 8, 15, 21, (3, 7), 0.6, False, False),       # 10x6 blocks, ragged tail
+    ("bf16", True, 1, 520, 8, 16, (2, 4), 0.5, True, False),      # 65 vectors per pixel
+    ("bf16", True, 1, 64, 1, 1, (1, 1), 1.0, True, True),         # 1x1 coarse: all edges
+    ("f32", False, 2, 16, 24, 32, (4, 8), 0.4, True, True),
+    ("f32", False, 1, 3, 7, 9, (7, 9), 0.5, False, False),        # 2x2 blocks
+])
+def test_upsample_add_parity(B, dtype, nhwc, n, c, hc, wc, grid, p, skip, relu):
+    r = synth.rng(300 + c + hc)
+    gh, gw = grid
+    coarse = synth.to_storage_bits(synth.normal(r, (n, c, hc, wc)), dtype)
+    sk = synth.to_storage_bits(synth.normal(r, (n, c, 2 * hc, 2 * wc)), dtype) if skip else None
+    prev = synth.nan_canaries(r, (n, c, 2 * hc, 2 * wc), dtype)
+    mask = synth.bernoulli_mask(r, n, gh, gw, p)
+    want = oracle.sparse_upsample_add(coarse, sk, mask, prev, dtype, relu)
+    idx, cnt = _index(B, mask)
+    out = to_dev(prev, dtype, nhwc)
+    lay = B.BC_NHWC if nhwc else B.BC_NCHW
+    B.bc_sparse_upsample_add(to_dev(coarse, dtype, nhwc), lay,
+                             to_dev(sk, dtype, nhwc) if skip else None, out, grid, int(relu),
+                             idx, cnt)
+    _check_merge(from_dev(out, nhwc), want, mask, dtype)
+
+
+def test_upsample_add_full_size(B):
+    """The largest merge of the decoder at 2048x1024: 128 channels, 128x256 -> 256x512,
+    32x32-pixel blocks of the 8x16 grid, 30 % of them executed."""
+    r = synth.rng(310)
+    dtype, n, c, hc, wc, gh, gw = "bf16", 1, 128, 128, 256, 8, 16
+    coarse = synth.to_storage_bits(synth.normal(r, (n, c, hc, wc)), dtype)
+    sk = synth.to_storage_bits(synth.normal(r, (n, c, 2 * hc, 2 * wc)), dtype)
+    prev = synth.nan_canaries(r, (n, c, 2 * hc, 2 * wc), dtype)
+    mask = synth.frac_mask(311, gh, gw, 0.3)
+    want = oracle.sparse_upsample_add(coarse, sk, mask, prev, dtype, True)
+    idx, cnt = _index(B, mask)
+    out = to_dev(prev, dtype)
+    B.bc_sparse_upsample_add(to_dev(coarse, dtype), B.BC_NHWC, to_dev(sk, dtype), out, (gh, gw), 1,
+                             idx, cnt)
+    _check_merge(from_dev(out), want, mask, dtype)
+
+
+def test_upsample_add_every_block_and_none(B):
+    r = synth.rng(320)
+    dtype, c, hc, wc, grid = "bf16", 32, 16, 32, (4, 8)
+    coarse = synth.to_storage_bits(synth.normal(r, (1, c, hc, wc)), dtype)
+    prev = synth.nan_canaries(r, (1, c, 2 * hc, 2 * wc), dtype)
+    full = np.ones((1,) + grid, np.uint8)
+    want = oracle.sparse_upsample_add(coarse, None, full, prev, dtype)
+    out = to_dev(prev, dtype)
+    B.bc_sparse_upsample_add(to_dev(coarse, dtype), B.BC_NHWC, None, out, grid, 0, None, None)
+    _check_merge(from_dev(out), want, full, dtype)
+    # an empty index leaves every block untouched
+    idx, cnt = _index(B, np.zeros((1,) + grid, np.uint8))
+    out = to_dev(prev, dtype)
+    B.bc_sparse_upsample_add(to_dev(coarse, dtype), B.BC_NHWC, None, out, grid, 0, idx, cnt)
+    assert np.array_equal(from_dev(out), prev)
+
+
+def test_upsample_of_constant_is_constant(B):
+    """Bilinear weights sum to one: a constant coarse map stays constant (exact in bf16)."""
+    coarse = torch.full((1, 8, 16, 16), 1.5, dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros((1, 16, 32, 16), dtype=torch.bfloat16, device="cuda")
+    B.bc_sparse_upsample_add(coarse, B.BC_NHWC, None, out, (2, 2), 0, None, None)
+    assert bool((out == 1.5).all())
+
+
+# ------------------------------------------------------------------ information gain, NHWC 16-bit
+
+def _ig_nhwc(B, lt_bits, lp_bits, dtype, classes, grid):
+    n = lt_bits.shape[0]
+    ig = torch.full((n,) + tuple(grid), -1.0, dtype=torch.float32, device="cuda")
+    B.bc_seg_information_gain(to_dev(lt_bits, dtype), to_dev(lp_bits, dtype), grid, ig,
+                              classes=classes, layout=B.BC_NHWC)
+    return ig.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype,n,classes,c,h,w,grid", [
+    ("bf16", 1, 19, 64, 64, 128, (8, 16)),      # a head padded to 64 output channels
+    ("bf16", 2, 19, 24, 40, 48, (4, 6)),
+    ("f16", 1, 5, 8, 32, 32, (2, 2)),
+    ("bf16", 1, 32, 32, 16, 48, (2, 3)),
+    ("f16", 1, 9, 16, 24, 24, (3, 3)),
+    ("bf16", 1, 1, 8, 16, 16, (2, 2)),          # one class: KL is 0
+])
+def test_information_gain_nhwc_parity(B, dtype, n, classes, c, h, w, grid):
+    r = synth.rng(330 + c + classes)
+    lt = synth.to_storage_bits(synth.seg_logits(r, n, classes, h, w, cell=8), dtype)
+    lp = synth.to_storage_bits(synth.seg_logits_next(r, synth.storage_to_f64(lt, dtype).astype(np.float32),
+                                                     changed=0.3, cell=16), dtype)
+    want = P.seg_information_gain(synth.storage_to_f64(lt, dtype), synth.storage_to_f64(lp, dtype), *grid)
+    pad = lambda b: np.concatenate([b, synth.nan_canaries(r, (n, c - classes, h, w), dtype)], axis=1)
+    got = _ig_nhwc(B, pad(lt), pad(lp), dtype, classes, grid)
+    assert max_abs_rel(got, want) <= 1e-4
+
+
+def test_information_gain_nhwc_full_size(B):
+    """19 classes in 64 channels at a quarter of 2048x1024 (512x256), 8x16 grid."""
+    r = synth.rng(340)
+    dtype, classes, c, h, w = "bf16", 19, 64, 256, 512
+    lt = synth.to_storage_bits(synth.seg_logits(r, 1, classes, h, w), dtype)
+    lp = synth.to_storage_bits(synth.seg_logits_next(r, synth.storage_to_f64(lt, dtype).astype(np.float32),
+                                                     changed=0.25), dtype)
+    want = P.seg_information_gain(synth.storage_to_f64(lt, dtype), synth.storage_to_f64(lp, dtype), 8, 16)
+    pad = lambda b: np.concatenate([b, synth.nan_canaries(r, (1, c - classes, h, w), dtype)], axis=1)
+    got = _ig_nhwc(B, pad(lt), pad(lp), dtype, classes, (8, 16))
+    assert max_abs_rel(got, want) <= 1e-4
+
+
+def test_information_gain_copied_blocks_are_zero(B):
+    """Blocks whose scores were transferred from frame t-1 have exactly zero gain."""
+    r = synth.rng(350)
+    dtype, classes, c, h, w, grid = "bf16", 19, 32, 64, 128, (4, 8)
+    lp = synth.to_storage_bits(synth.seg_logits(r, 1, c, h, w), dtype)
+    fresh = synth.to_storage_bits(synth.seg_logits(r, 1, c, h, w), dtype)
+    mask = synth.bernoulli_mask(r, 1, *grid, 0.5)
+    lt = oracle.select(mask, fresh, lp, h // grid[0], w // grid[1])
+    got = _ig_nhwc(B, lt, lp, dtype, classes, grid)
+    assert (got[mask == 0] == 0.0).all()
+    want = P.seg_information_gain(synth.storage_to_f64(lt[:, :classes], dtype),
+                                  synth.storage_to_f64(lp[:, :classes], dtype), *grid)
+    assert max_abs_rel(got, want) <= 1e-4
