@@ -1,4 +1,5 @@
-"""Frame-by-frame block-sparse ResNet backbones with persistent per-layer buffers.
+"""Frame-by-frame block-sparse ResNet backbones and SwiftNet-style segmentation
+networks with persistent per-layer buffers.
 
 Single-stage networks make every convolution block-sparse (Section 4); all layers of
 a frame use the frame's one execution grid (Section 3.5); each layer's output is a
@@ -9,8 +10,17 @@ BlockCopy configuration). Layers run in network order on one HIP stream.
 Backbones: ResNet-18 (basic blocks [2, 2, 2, 2]) and ResNet-50 (bottlenecks
 [3, 4, 6, 3], stride on the 3x3 convolution), 7x7/2 stem and 3x3/2 max pooling,
 batch norm folded into the convolutions (bc_fold_bn), no classifier. All feature
-maps are channels-last bf16 (or fp16). Work per frame: one bc_build_block_index and
-one library call per layer; nothing runs on the host in between.
+maps are channels-last bf16 (or fp16). Work per frame: one bc_build_block_index (or an
+index handed in, e.g. from bc_sample_execution_grid) and one library call per layer;
+nothing runs on the host in between.
+
+Segmentation network (Section 4: a SwiftNet-style single-scale model): the backbone as
+encoder, then a decoder from stride 32 up to stride 4 in which every level upsamples
+the coarser decoder feature by two (bc_sparse_upsample_add), adds a 1x1 projection of
+the encoder feature at that stride and blends with a 3x3 convolution; a 1x1 head gives
+the class scores at stride 4. The stride-32 context module is a 1x1 projection here
+(pooling over the whole image does not decompose into blocks), and the head computes
+64 channels per started 64 classes, the first `classes` being the scores.
 """
 from __future__ import annotations
 
@@ -24,7 +34,7 @@ from . import bc
 
 @dataclass
 class Layer:
-    kind: str                  # "conv" or "pool"
+    kind: str                  # "conv", "pool" or "up" (upsample src by 2, add res)
     name: str
     src: int                   # producing layer, -1 = the frame
     cin: int
@@ -72,6 +82,32 @@ def build_layers(depth: int) -> list[Layer]:
     return L
 
 
+def build_swiftnet_layers(depth: int = 18, classes: int = 19, width: int = 128) -> list[Layer]:
+    """Encoder (the backbone of build_layers) followed by the decoder, in execution
+    order: dec.proj4 (1x1 on the stride-32 output), then per level s = 3, 2, 1 the
+    lateral dec.lat{s} (1x1 on the last output of encoder stage s), dec.up{s}
+    (coarser decoder feature upsampled by two plus the lateral) and dec.blend{s} (3x3);
+    then dec.logits (1x1, no ReLU)."""
+    L = build_layers(depth)
+    grow = 4 if depth == 50 else 1
+    last = {}
+    for i, l in enumerate(L):
+        if l.name.startswith("layer"):
+            last[int(l.name[len("layer")])] = i          # ends on the stage's last layer
+
+    def add(layer: Layer) -> int:
+        L.append(layer)
+        return len(L) - 1
+
+    x = add(Layer("conv", "dec.proj4", last[4], 512 * grow, width, 1, 1))
+    for s in (3, 2, 1):
+        lat = add(Layer("conv", f"dec.lat{s}", last[s], (32 << s) * grow, width, 1, 1))
+        up = add(Layer("up", f"dec.up{s}", x, width, width, 1, 1, relu=False, res=lat))
+        x = add(Layer("conv", f"dec.blend{s}", up, width, width, 3, 1))
+    add(Layer("conv", "dec.logits", x, width, 64 * -(-classes // 64), 1, 1, relu=False))
+    return L
+
+
 def default_params(layers: list[Layer], seed0: int = 1000, bn_random: bool = False):
     """He-normal fp32 OIHW weights (seed seed0 + layer position) and batch-norm
     statistics (identity unless bn_random), drawn by the shared input generators."""
@@ -98,6 +134,9 @@ def layer_shapes(layers: list[Layer], h: int, w: int) -> list[tuple[int, int, in
     shapes = []
     for l in layers:
         ih, iw = (h, w) if l.src < 0 else shapes[l.src][:2]
+        if l.kind == "up":
+            shapes.append((2 * ih, 2 * iw, l.cout))
+            continue
         shapes.append(((ih + 2 * l.pad - l.k) // l.stride + 1,
                        (iw + 2 * l.pad - l.k) // l.stride + 1, l.cout))
     return shapes
@@ -131,11 +170,12 @@ class SparseResNet:
     """
 
     def __init__(self, depth: int, h: int, w: int, block: int = 128, params=None,
-                 dtype=torch.bfloat16, device="cuda", seed0: int = 1000, bn_random: bool = False):
+                 dtype=torch.bfloat16, device="cuda", seed0: int = 1000, bn_random: bool = False,
+                 layers: list[Layer] | None = None):
         if h % block or w % block or block % 32:
             raise ValueError("frame size must be a multiple of the block size, and the block "
                              "size a multiple of 32 (the backbone's total stride)")
-        self.layers = build_layers(depth)
+        self.layers = layers if layers is not None else build_layers(depth)
         self.h, self.w, self.block = h, w, block
         self.grid = (h // block, w // block)
         self.dtype, self.device = dtype, torch.device(device)
@@ -181,10 +221,13 @@ class SparseResNet:
         m = torch.as_tensor(np.asarray(mask, np.uint8) if not torch.is_tensor(mask) else mask)
         self.mask.copy_(m.reshape(self.mask.shape), non_blocking=False)
 
-    def frame(self, x, sparse: bool = True, stream=None):
+    def frame(self, x, sparse: bool = True, stream=None, index=None):
         """Run one frame. x: [1, h, w, 3] channels-last on the device. sparse=False runs
-        every block (first frame of a clip); sparse=True uses the grid in self.mask."""
-        if sparse:
+        every block (first frame of a clip); sparse=True uses the grid in self.mask, or
+        the device (idx, count) pair `index` if given (then self.mask is not read)."""
+        if sparse and index is not None:
+            idx, cnt = index
+        elif sparse:
             bc.bc_build_block_index(self.mask, 1, self.grid, self.idx, self.count, stream=stream)
             idx, cnt = self.idx, self.count
         else:
@@ -200,8 +243,27 @@ class SparseResNet:
         if l.kind == "pool":
             bc.bc_sparse_maxpool2d((l.k, l.k, l.stride, l.pad, 0), src, bc.BC_NHWC, out, self.grid,
                                    idx, cnt, stream)
+        elif l.kind == "up":
+            bc.bc_sparse_upsample_add(src, bc.BC_NHWC, self.buffers[l.res], out, self.grid,
+                                      int(l.relu), idx, cnt, stream)
         else:
             res = None if l.res is None else self.buffers[l.res]
             bc.bc_sparse_conv2d((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC,
                                 self.weights[i], self.biases[i], res, out, self.grid, idx, cnt,
                                 stream)
+
+
+class SparseSwiftNet(SparseResNet):
+    """SwiftNet-style segmentation network (encoder = ResNet backbone, decoder of
+    build_swiftnet_layers) executed block-sparsely frame by frame. `logits` is the
+    persistent stride-4 score buffer [1, h/4, w/4, 64*ceil(classes/64)] whose first
+    `classes` channels are the class scores."""
+
+    def __init__(self, depth: int, h: int, w: int, block: int = 128, classes: int = 19,
+                 width: int = 128, **kw):
+        self.classes = classes
+        super().__init__(depth, h, w, block, layers=build_swiftnet_layers(depth, classes, width), **kw)
+
+    @property
+    def logits(self):
+        return self.buffers[-1]

@@ -263,9 +263,9 @@ def test_repack_host_matches_oracle_rounding(B):
 def test_runner_table_matches_oracle_table():
     from oracle import network as onet
     from paper_2108_09376_amd import resnet
-    for depth in (18, 50):
-        a = onet.resnet_table(depth)
-        b = resnet.build_layers(depth)
+    pairs = [(onet.resnet_table(d), resnet.build_layers(d)) for d in (18, 50)]
+    pairs += [(onet.swiftnet_table(d), resnet.build_swiftnet_layers(d)) for d in (18, 50)]
+    for a, b in pairs:
         assert len(a) == len(b)
         for x, y in zip(a, b):
             assert (x["kind"], x["cin"], x["cout"], x["k"], x["stride"], x["pad"], x["relu"], x["src"], x["res"]) == \

@@ -16,6 +16,7 @@ import torch
 import oracle
 import synth
 from oracle import network as onet
+from oracle import policy as P
 from tests._util import block_select, from_dev, max_abs_rel, to_dev, weights_dev
 
 pytestmark = pytest.mark.gpu
@@ -39,8 +40,14 @@ def _norm_rel(g, r):
     return float(np.linalg.norm(g - r) / max(1e-30, np.linalg.norm(r)))
 
 
-@pytest.mark.parametrize("depth", [18, 50])
-def test_runner_matches_oracle_network(R, depth):
+def _net(resnet, kind, depth, h, w, **kw):
+    if kind == "swiftnet":
+        return resnet.SparseSwiftNet(depth, h, w, 128, **kw)
+    return resnet.SparseResNet(depth, h, w, 128, **kw)
+
+
+@pytest.mark.parametrize("kind,depth", [("resnet", 18), ("resnet", 50), ("swiftnet", 18)])
+def test_runner_matches_oracle_network(R, kind, depth):
     """End to end, no value from the GPU fed back to the oracle. Every layer stores bf16,
     so a GPU sum that lands on the other side of a rounding boundary than the fp64 sum
     (about 1e-4 of the outputs per layer, 1 ulp each) propagates to later layers. The
@@ -50,10 +57,10 @@ def test_runner_matches_oracle_network(R, depth):
     perturbations grow without bound."""
     bc, resnet = R
     h, w = 256, 512
-    table = onet.resnet_table(depth)
+    table = onet.swiftnet_table(depth) if kind == "swiftnet" else onet.resnet_table(depth)
     params = _params(table, bn_random=False)
     folded = onet.fold_params(table, params, "bf16")
-    net = resnet.SparseResNet(depth, h, w, 128, params=params)
+    net = _net(resnet, kind, depth, h, w, params=params)
     x0 = synth.to_storage_bits(synth.normal(synth.rng(1), (1, 3, h, w)), "bf16")
     x1 = synth.to_storage_bits(synth.normal(synth.rng(11), (1, 3, h, w)), "bf16")
     mask = np.array([[[1, 0, 1, 1], [0, 1, 0, 0]]], np.uint8)
@@ -83,10 +90,12 @@ def test_runner_matches_oracle_network(R, depth):
     assert max(max(r[2], r[3]) for r in rows) <= 2e-2
 
 
-@pytest.mark.parametrize("depth,h,w", [(18, 256, 512), (50, 256, 512), (50, 1024, 2048)])
-def test_runner_static_frame_bit_identical(R, depth, h, w):
+@pytest.mark.parametrize("kind,depth,h,w", [("resnet", 18, 256, 512), ("resnet", 50, 256, 512),
+                                            ("resnet", 50, 1024, 2048), ("swiftnet", 18, 256, 512),
+                                            ("swiftnet", 18, 1024, 2048)])
+def test_runner_static_frame_bit_identical(R, kind, depth, h, w):
     bc, resnet = R
-    net = resnet.SparseResNet(depth, h, w, 128, bn_random=True)
+    net = _net(resnet, kind, depth, h, w, bn_random=True)
     x = _frame_dev(synth.to_storage_bits(synth.normal(synth.rng(1), (1, 3, h, w)), "bf16"))
     net.frame(x, sparse=False)
     torch.cuda.synchronize()
@@ -139,6 +148,54 @@ def test_runner_refuses_sparse_frame_before_full_frame(R):
         net.frame(x, sparse=True)
     assert e.value.status == bc.BC_ERR_UNINITIALIZED
     torch.cuda.synchronize()
+
+
+def test_blockcopy_step_on_swiftnet(R):
+    """One BlockCopy step after a full first frame, all on the device: execution grid
+    sampled from the policy's probabilities (bit for bit against the oracle's
+    sampling), frame state updated (bit for bit), the segmentation network run on the
+    sampled index, information gain of the new class scores against the saved previous
+    ones, rewards. Checked against oracle-only values: blocks that did not run copied
+    their scores, so their gain is exactly 0 and their reward -gamma (tau - M_t); the
+    cost and moving average follow from the oracle's grid."""
+    bc, resnet = R
+    h, w, tau, gamma, mu, seed, t = 256, 512, 0.3, 5.0, 0.9, 77, 1
+    net = resnet.SparseSwiftNet(18, h, w, 128)
+    gh, gw = net.grid
+    prob = synth.block_probabilities(synth.rng(60), 1, gh, gw)
+    want_mask, want_idx = P.sample_execution_grid(prob, seed, t)
+    assert 0 < want_mask.sum() < want_mask.size
+    b0 = synth.to_storage_bits(synth.normal(synth.rng(61), (1, 3, h, w)), "bf16")
+    b1 = synth.to_storage_bits(synth.normal(synth.rng(62), (1, 3, h, w)), "bf16")
+    x0, x1 = _frame_dev(b0), _frame_dev(b1)
+    net.frame(x0, sparse=False)                      # frame 0: every block
+    state = x0.clone()
+    prev_logits = torch.empty_like(net.logits)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    p, mask = dev(prob), torch.empty((1, gh, gw), dtype=torch.uint8, device="cuda")
+    idx = torch.full((gh * gw,), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    ig = torch.full((1, gh, gw), -1.0, device="cuda")
+    mavg = torch.full((1,), 0.5, device="cuda")
+    reward, cost, loss = torch.empty((1, gh, gw), device="cuda"), torch.empty(1, device="cuda"), torch.empty(1, device="cuda")
+    # the step
+    bc.bc_sample_execution_grid(p, net.grid, seed, t, mask, idx, cnt)
+    bc.bc_update_frame_state(x1, state, bc.BC_NHWC, net.grid, idx, cnt)
+    bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, net.grid, None, None)
+    net.frame(x1, sparse=True, index=(idx, cnt))
+    bc.bc_seg_information_gain(net.logits, prev_logits, net.grid, ig, classes=net.classes, layout=bc.BC_NHWC)
+    bc.bc_block_rewards(ig, mask, p, net.grid, tau, gamma, mu, mavg, reward, cost, loss)
+    torch.cuda.synchronize()
+    m = mask.cpu().numpy()
+    assert np.array_equal(m, want_mask)
+    assert np.array_equal(idx.cpu().numpy()[:want_idx.size], want_idx) and int(cnt.item()) == want_idx.size
+    assert np.array_equal(from_dev(state), P.update_frame_state(b1, b0, want_mask, "nchw"))
+    g = ig.cpu().numpy()
+    assert (g[want_mask == 0] == 0.0).all() and (g[want_mask == 1] > 0.0).all()
+    _, want_c, want_m = P.block_rewards(np.zeros_like(g, np.float64), want_mask, tau, gamma, mu, [0.5])
+    assert abs(float(cost.item()) - want_c[0]) <= 1e-6 and abs(float(mavg.item()) - want_m[0]) <= 1e-6
+    rw = reward.cpu().numpy().astype(np.float64)
+    assert max_abs_rel(rw[want_mask == 0], -gamma * (tau - want_m[0])) <= 1e-5
 
 
 # ------------------------------------------------------------------ full-size layers
