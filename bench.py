@@ -42,7 +42,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch layer by layer instead of a HIP graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-scatter", action="store_true")
-    ap.add_argument("--no-clip", action="store_true", help="skip the ResNet-18 30-frame clip")
+    ap.add_argument("--no-clip", action="store_true",
+                    help="skip the 30-frame clip (ResNet-18 encoder; SwiftNet-18 full step)")
     ap.add_argument("--no-policy-steps", action="store_true",
                     help="skip sampling / frame state / information gain / rewards")
     ap.add_argument("--pmc-frames", type=int, default=0,
@@ -237,7 +238,14 @@ def policy_steps(torch, bc, dev):
       seg_information_gain  19-class fp32 scores of frame t and t-1 (2 x 159 MB read,
                         more than the 256 MB last-level cache holds), per-pixel KL and
                         block max; algorithmic bytes = both score maps once
-      block_rewards     rewards, cost, moving average and loss over 128 blocks"""
+      block_rewards     rewards, cost, moving average and loss over 128 blocks
+      seg_information_gain_nhwc  the segmentation network's own output: bf16 scores at
+                        stride 4 (512x256), 19 classes in 64 channels; algorithmic bytes
+                        = the 19 class scores of both maps once
+      upsample_add      the decoder's largest merge (128x256 -> 256x512, 128 channels,
+                        bf16, skip added, 38 blocks); algorithmic bytes = the active
+                        blocks' coarse tiles with their one-pixel halo and skip read
+                        once, the output blocks written once"""
     import numpy as np
 
     import synth
@@ -255,6 +263,11 @@ def policy_steps(torch, bc, dev):
     lt = torch.from_numpy(synth.seg_logits(r, 1, 19, 1024, 2048)).to(dev)
     lp = (lt + 0.1 * torch.randn_like(lt)).contiguous()
     ig = torch.empty((1, 8, 16), dtype=torch.float32, device=dev)
+    lt4 = torch.randn((1, 256, 512, 64), device=dev).mul_(4).to(torch.bfloat16)
+    lp4 = (lt4.float() + 0.1 * torch.randn_like(lt4, dtype=torch.float32)).to(torch.bfloat16)
+    coarse = torch.randn((1, 128, 256, 128), device=dev).to(torch.bfloat16)
+    skip = torch.randn((1, 256, 512, 128), device=dev).to(torch.bfloat16)
+    upout = torch.zeros_like(skip)
     mavg = torch.full((1,), 0.3, device=dev)
     reward = torch.empty((1, 8, 16), device=dev)
     cost = torch.empty(1, device=dev)
@@ -267,6 +280,12 @@ def policy_steps(torch, bc, dev):
                                  2 * 19 * 1024 * 2048 * 4),
         "block_rewards": (lambda: bc.bc_block_rewards(ig, mask, prob, (8, 16), 0.3, 5.0, 0.9, mavg, reward,
                                                       cost, loss), None),
+        "seg_information_gain_nhwc": (lambda: bc.bc_seg_information_gain(lt4, lp4, (8, 16), ig, classes=19,
+                                                                         layout=bc.BC_NHWC),
+                                      2 * 19 * 256 * 512 * 2),
+        "upsample_add": (lambda: bc.bc_sparse_upsample_add(coarse, bc.BC_NHWC, skip, upout, (8, 16), 0,
+                                                           idx38, cnt38),
+                         38 * 128 * 2 * ((16 + 2) * (16 + 2) + 2 * 32 * 32)),
     }
     out = {}
     for name, (fn, nbytes) in ops.items():
@@ -341,6 +360,103 @@ def resnet18_clip(torch, dev, frames=30):
             "mean_active_fraction": round(float(np.mean(fracs)), 4),
             "effective_TFLOPs": round(flops / (ms * 1e-3) / 1e12, 2),
             "launch": "one HIP graph replay per sparse frame"}
+
+
+def swiftnet_clip_step(torch, bc, dev, frames=30, seed=2021):
+    """The whole BlockCopy step per frame on the same 30-frame clip, with the SwiftNet-18
+    segmentation network (ResNet-18 encoder + decoder, 19 classes, random init, bf16):
+      1. execution grid sampled from the policy's block probabilities, index built
+         (bc_sample_execution_grid);
+      2. frame state: executed blocks of the RGB frame copied (bc_update_frame_state);
+      3. the previous class scores saved (a full-buffer bc_update_frame_state);
+      4. the sparse network on the sampled index (42 layers incl. 3 upsample merges);
+      5. information gain of the stride-4 scores (19 of 64 channels) against the saved
+         ones (bc_seg_information_gain);
+      6. rewards, cost, moving average and REINFORCE loss (bc_block_rewards).
+    The policy network is not part of the step: its stand-in output is p = 1 on the
+    blocks the clip's objects touch at t or t-1 and 0.05 elsewhere (exploration),
+    copied in with the frame. One HIP graph replay per frame; the graph fixes the
+    generator's counter, so frames differ through their probabilities only. Also timed:
+    the network alone (step 4) on the same grids, and the steps around it (1-3, 5, 6)
+    alone, each replayed as its own graph."""
+    import numpy as np
+
+    import synth
+    from paper_2108_09376_amd import resnet
+    clip = synth.SyntheticClip(synth.SEED_INPUT + 4)
+    net = resnet.SparseSwiftNet(18, 1024, 2048, 128, device=dev)
+    grid = net.grid
+    gh, gw = grid
+    x = torch.empty((1, 1024, 2048, 3), dtype=torch.bfloat16, device=dev)
+    state = torch.empty_like(x)
+    prob = torch.empty((1, gh, gw), dtype=torch.float32, device=dev)
+    mask = torch.empty((1, gh, gw), dtype=torch.uint8, device=dev)
+    idx = torch.empty(gh * gw, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    prev_logits = torch.empty_like(net.logits)
+    ig = torch.empty((1, gh, gw), dtype=torch.float32, device=dev)
+    mavg = torch.full((1,), 0.3, device=dev)
+    reward = torch.empty((1, gh, gw), device=dev)
+    cost, loss = torch.empty(1, device=dev), torch.empty(1, device=dev)
+
+    def load(t):
+        img = synth.to_storage_bits(clip.frame(t), "bf16")
+        x.copy_(torch.from_numpy(img.view(np.int16)).view(torch.bfloat16))
+        prob.copy_(torch.from_numpy(np.where(clip.mask(t) != 0, 1.0, 0.05).astype(np.float32)))
+        torch.cuda.synchronize()
+
+    def before():
+        bc.bc_sample_execution_grid(prob, grid, seed, 1, mask, idx, cnt)
+        bc.bc_update_frame_state(x, state, bc.BC_NHWC, grid, idx, cnt)
+        bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, grid, None, None)
+
+    def network():
+        net.frame(x, sparse=True, index=(idx, cnt))
+
+    def after():
+        bc.bc_seg_information_gain(net.logits, prev_logits, grid, ig, classes=net.classes,
+                                   layout=bc.BC_NHWC)
+        bc.bc_block_rewards(ig, mask, prob, grid, 0.3, 5.0, 0.9, mavg, reward, cost, loss)
+
+    def restart():
+        load(0)
+        net.frame(x, sparse=False)        # frame 0: every block
+        state.copy_(x)
+        torch.cuda.synchronize()
+
+    restart()
+    graphs = {}
+    for name, fns in (("step", (before, network, after)), ("network", (network,)),
+                      ("around", (before, after))):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for fn in fns:
+                fn()
+        graphs[name] = g
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res = {}
+    for name in ("step", "network", "around"):
+        restart()                         # the captures ran nothing; every pass starts the clip anew
+        times, fracs = [], []
+        for t in range(1, frames):
+            load(t)
+            if name == "network":         # the grid the step would sample, outside the timing
+                bc.bc_sample_execution_grid(prob, grid, seed, 1, mask, idx, cnt)
+            e0.record()
+            graphs[name].replay()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+            fracs.append(float(mask.float().mean().item()))
+        res[name] = (float(np.mean(times)), float(np.mean(fracs)))
+    ms, frac = res["step"]
+    flops = net.conv_flops(int(round(frac * gh * gw)))
+    return {"frames": frames, "network": "SwiftNet-18 (ResNet-18 encoder + 3-level decoder), 19 classes",
+            "mean_ms_per_step": round(ms, 4), "mean_ms_network_only": round(res["network"][0], 4),
+            "mean_ms_steps_around_network": round(res["around"][0], 4),
+            "mean_active_fraction": round(frac, 4),
+            "effective_TFLOPs_network_in_step": round(flops / (ms * 1e-3) / 1e12, 2),
+            "launch": "one HIP graph replay per step"}
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "sparse_conv_traffic_resnet50_2048x1024_active0.3.txt")
@@ -630,6 +746,7 @@ def main():
         out["gather_scatter"] = gather_scatter(torch, bc, dev)
     if not args.no_clip:
         out["resnet18_clip"] = resnet18_clip(torch, dev)
+        out["swiftnet18_clip_step"] = swiftnet_clip_step(torch, bc, dev)
     if not args.no_policy_steps:
         out["policy_steps"] = policy_steps(torch, bc, dev)
     if not args.no_cpu_baseline:

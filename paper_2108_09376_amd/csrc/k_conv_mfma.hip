@@ -445,6 +445,69 @@ constexpr int kMaxSplitTiles = 1 << 16;
 constexpr int kMaxSplit = 4;        // K slices per tile
 __device__ uint32_t g_split_counter[kMaxSplitTiles];   // zero at load, reset after use
 
+// Split-K hand-off: every K slice of a tile stores its fp32 partial (the four waves'
+// MI x NI fragments), and the last slice to arrive (per-tile counter) adds all
+// partials in slice order 0, 1, ... into `acc` and returns true; the others return
+// false and exit. Partials are written through to the device-coherent level
+// (agent-scope atomic stores), all of this workgroup's stores are waited for before
+// the counter is incremented, and the last slice reads the others' partials with
+// agent-scope loads, so no cache-wide write-back or invalidate is needed. The last
+// slice resets the counter, so no memset is needed between calls (safe under graph
+// replay).
+template <int MI, int NI>
+__device__ __forceinline__ bool split_k_handoff(const MfmaArgs &a, f32x4 (&acc)[MI][NI], int tile,
+                                                int ks, int *s_last)
+{
+    constexpr int SLICE = 4 * MI * NI * 64 * 4;     // floats of one slice's partial tile
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float *base = a.ws + (size_t)tile * a.ksplit * SLICE;
+    float *mine = base + (size_t)ks * SLICE;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                __hip_atomic_store(mine + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4 + i,
+                                   acc[mi][ni][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0)
+        *s_last = __hip_atomic_fetch_add(&g_split_counter[tile], 1u, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(a.ksplit - 1);
+    __syncthreads();
+    if (!*s_last) return false;
+    // request every other slice's partial first, then add in slice order 0, 1, ...
+    f32x4 part[kMaxSplit][MI][NI];
+#pragma unroll
+    for (int sl = 0; sl < kMaxSplit; ++sl) {
+        if (sl >= a.ksplit || sl == ks) continue;
+        const float *src = base + (size_t)sl * SLICE;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+                const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    part[sl][mi][ni][i] = __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+    }
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) {
+            f32x4 tot = (ks == 0) ? acc[mi][ni] : part[0][mi][ni];
+#pragma unroll
+            for (int sl = 1; sl < kMaxSplit; ++sl)
+                if (sl < a.ksplit) tot += (sl == ks) ? acc[mi][ni] : part[sl][mi][ni];
+            acc[mi][ni] = tot;
+        }
+    if (tid == 0)
+        __hip_atomic_store(&g_split_counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
 // Halo vectors (16 bytes) each thread stages per chunk: the halo of a 64-row tile has at
 // most 192 slots at stride 1 and 384 at stride 2 (a 128-row tile: 704). Every vector
 // costs a load instruction even when it falls outside the halo, so the bound is kept
@@ -472,6 +535,32 @@ struct RingSteps<D, D> {
     template <class F>
     __device__ __forceinline__ static void run(F &, int, int) {}
 };
+
+// Runs a ring of D steps over n steps: a loop of whole rings (no exit inside, so the
+// loop's back edge only carries the state after the last slot, and the compiler's wait
+// counting sees every slot's requests at their true age), then the partial ring.
+template <int I, int D>
+struct RingAll {
+    template <class F>
+    __device__ __forceinline__ static void run(F &f, int j)
+    {
+        f(std::integral_constant<int, I>{}, j + I);
+        RingAll<I + 1, D>::run(f, j);
+    }
+};
+template <int D>
+struct RingAll<D, D> {
+    template <class F>
+    __device__ __forceinline__ static void run(F &, int) {}
+};
+
+template <int D, class F>
+__device__ __forceinline__ void ring_loop(F &f, int n)
+{
+    int j = 0;
+    for (; j + D <= n; j += D) RingAll<0, D>::run(f, j);
+    RingSteps<0, D>::run(f, j, n);
+}
 
 // SG (stage grouping) sets how much of K one barrier covers: one tap (SG = 1) or all KT
 // taps of a 32-channel chunk (SG = KT, 3x3 layers only).
@@ -618,7 +707,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
             load_a(c_lo + j + D, ra[d]);
             compute(sa, sb, 0);
         };
-        for (int j = 0; j < nsteps; j += D) RingSteps<0, D>::run(step, j, nsteps);
+        ring_loop<D>(step, nsteps);
     } else if constexpr (SG == 1) {
         // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
         // while the current chunk is multiplied
@@ -672,63 +761,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
             for (int t = 0; t < KT; ++t)
                 compute(sa, sb + t * BN * PITCH, ((t / KS) * a.HC + (t % KS)) * PITCH);
         };
-        for (int cj = 0; cj < nch; cj += D) RingSteps<0, D>::run(step, cj, nch);
+        ring_loop<D>(step, nch);
     }
 
-    if constexpr (BM == 64 && BN == 64) if (a.ksplit > 1) {
-        // Hand the partial tile to the last slice. Partials are written through to the
-        // device-coherent level (agent-scope atomic stores), all of this workgroup's
-        // stores are waited for before the per-tile counter is incremented, and the last
-        // slice reads the others' partials with agent-scope loads, so no cache-wide
-        // write-back or invalidate is needed.
-        const int tile = mt * a.ntn + nt;
-        float *base = a.ws + (size_t)tile * a.ksplit * (BM * BN);
-        float *mine = base + (size_t)ks * (BM * BN);
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    __hip_atomic_store(mine + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4 + i,
-                                       acc[mi][ni][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (tid == 0)
-            s_last = __hip_atomic_fetch_add(&g_split_counter[tile], 1u, __ATOMIC_RELAXED,
-                                            __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(a.ksplit - 1);
-        __syncthreads();
-        if (!s_last) return;
-        // request every other slice's partial first, then add in slice order 0, 1, ...
-        f32x4 part[kMaxSplit][MI][NI];
-#pragma unroll
-        for (int sl = 0; sl < kMaxSplit; ++sl) {
-            if (sl >= a.ksplit || sl == ks) continue;
-            const float *src = base + (size_t)sl * (BM * BN);
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < NI; ++ni) {
-                    const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        part[sl][mi][ni][i] =
-                            __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-        }
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-                f32x4 tot = (ks == 0) ? acc[mi][ni] : part[0][mi][ni];
-#pragma unroll
-                for (int sl = 1; sl < kMaxSplit; ++sl)
-                    if (sl < a.ksplit) tot += (sl == ks) ? acc[mi][ni] : part[sl][mi][ni];
-                acc[mi][ni] = tot;
-            }
-        if (tid == 0)
-            __hip_atomic_store(&g_split_counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if constexpr (BM == 64 && BN == 64)
+        if (a.ksplit > 1 && !split_k_handoff(a, acc, mt * a.ntn + nt, ks, &s_last)) return;
     epi.finish(a, acc, smem, n0);
 }
 
@@ -1071,8 +1108,8 @@ std::map<const void *, size_t> g_attr_lds;   // dynamic LDS each kernel has opte
 template <typename K>
 hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
 {
-    if (p.lds > 64 * 1024) {
-        // opt in to more than 64 KB of dynamic LDS (gfx950: 160 KB per workgroup, static
+    if (p.lds >= 60 * 1024) {
+        // opt in to 60 KB or more of dynamic LDS (gfx950: 160 KB per workgroup, static
         // shared memory included), raised per kernel to the largest size launched so far
         std::lock_guard<std::mutex> lk(g_attr_mu);
         size_t &cur = g_attr_lds[(const void *)kernel];

@@ -6,7 +6,7 @@
 //
 // All of these are small or streaming kernels: the sampling and the rewards touch one
 // value per block, the frame state copies the executed blocks of the RGB frame, and
-// the information gain streams two [n][classes][h][w] fp32 score maps once (HBM bound).
+// the information gain streams the class scores of two score maps once (HBM bound).
 #include "bc_internal.h"
 
 namespace bc {
@@ -276,8 +276,9 @@ __device__ __forceinline__ void block_max_out(float best, float *wave_max, float
 }
 
 // Channels first, fp32: one workgroup covers `rows` image rows of one block (about
-// kIgPixPerWG pixels); per pixel all 2*classes scores are requested at once (raw buffer
-// loads, classes past the count return zero and are left out of every sum).
+// kIgPixPerWG pixels, or a quarter of that); per pixel all 2*classes scores are
+// requested at once (raw buffer loads, classes past the count return zero and are left
+// out of every sum).
 template <int CMAX>
 __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
     const float *__restrict__ lt, const float *__restrict__ lp, IgGeom g, float *__restrict__ ig)
@@ -481,7 +482,10 @@ hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, in
     IgGeom g;
     g.classes = classes; g.c = c; g.h = h; g.w = w; g.gh = gh; g.gw = gw;
     const int bh = h / gh, bw = w / gw;
-    g.rows = kIgPixPerWG / bw;
+    // about kIgPixPerWG pixels per workgroup, a quarter of that below 2M pixels (a
+    // quarter-resolution score map) so that the launch still has >= 512 workgroups
+    const int per_wg = (long long)n * h * w >= (1LL << 21) ? kIgPixPerWG : kIgPixPerWG / 4;
+    g.rows = per_wg / bw;
     g.rows = g.rows < 1 ? 1 : (g.rows > bh ? bh : g.rows);
     g.strips = (bh + g.rows - 1) / g.rows;
     g.bytes = (int)((size_t)c * h * w * esize);   // one image's scores (checked < 2 GiB)
