@@ -33,7 +33,6 @@
 // The stem form handles layers with few input channels (kw * Cin <= 32, e.g. the
 // 7x7 RGB stem): K is ordered (kernel row i, then the kw*Cin values of that row,
 // which are contiguous in a channels-last row), one MFMA k step per kernel row.
-#include <array>
 #include <mutex>
 #include <map>
 #include <set>
@@ -565,7 +564,7 @@ __device__ __forceinline__ void ring_loop(F &f, int n)
 
 // SG (stage grouping) sets how much of K one barrier covers: one tap (SG = 1) or all KT
 // taps of a 32-channel chunk (SG = KT, 3x3 layers only).
-template <bool BF16, int BM, int BN, int KS, int S, int SG, bool PERSIST>
+template <bool BF16, int BM, int BN, int KS, int S, int SG>
 __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 {
     constexpr int SS = (KS == 1) ? S : 1;
@@ -582,207 +581,192 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1, q = tid & 3;
     // natural tile order L = (mt * ntn + nt) * ksplit + ks: N tile and K slice are known
-    // without the active count, and the live tiles come first. Returns false for a tile
-    // beyond the active count.
-    auto run_tile = [&](const int L) -> bool {
-        const int ks = L % a.ksplit;
-        const int mn = L / a.ksplit;
-        const int nt = mn % a.ntn;
-        const int mt = mn / a.ntn;
-        const int n0 = nt * BN;
-        const int nchunk = (a.cin + BK - 1) / BK;
-        const int c_lo = ks * a.cps;
-        const int c_hi = min(nchunk, c_lo + a.cps);
-        const int nsteps = (c_hi - c_lo) * KT;
+    // without the active count
+    const int L = blockIdx.x;
+    const int ks = L % a.ksplit;
+    const int mn = L / a.ksplit;
+    const int nt = mn % a.ntn;
+    const int mt = mn / a.ntn;
+    const int n0 = nt * BN;
+    const int nchunk = (a.cin + BK - 1) / BK;
+    const int c_lo = ks * a.cps;
+    const int c_hi = min(nchunk, c_lo + a.cps);
+    const int nsteps = (c_hi - c_lo) * KT;
 
-        // Every request is issued unconditionally as a raw buffer load: lanes without data
-        // (zero padding, inactive patches, channels past Cin, steps past the slice) use an
-        // offset beyond the buffer, for which the hardware returns zeros. The loops below
-        // are therefore straight-line code and the compiler can wait for exactly the request
-        // a step needs instead of draining every outstanding one. Requests return in issue
-        // order, so they are issued in the order they are needed: halo, weights, epilogue.
-        if (!load_tile_blocks(a, mt, tb)) return false;   // beyond the active count (uniform)
-        const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
-        const int wq = ((n0 + (tid >> 2)) * KT * a.cin + q * 8) * 2;   // byte offset, tap 0 chunk 0
-        auto load_b = [&](int j, uint4 (&r)[BV]) {
-            const int c = c_lo + j / KT, tap = j - (j / KT) * KT;
-            const bool ok = j < nsteps && c * BK + q * 8 < a.cin;
+    // Every request is issued unconditionally as a raw buffer load: lanes without data
+    // (zero padding, inactive patches, channels past Cin, steps past the slice) use an
+    // offset beyond the buffer, for which the hardware returns zeros. The loops below
+    // are therefore straight-line code and the compiler can wait for exactly the request
+    // a step needs instead of draining every outstanding one. Requests return in issue
+    // order, so they are issued in the order they are needed: halo, weights, epilogue.
+    if (!load_tile_blocks(a, mt, tb)) return;   // tile beyond the active count (uniform)
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
+    const int wq = ((n0 + (tid >> 2)) * KT * a.cin + q * 8) * 2;   // byte offset, tap 0 chunk 0
+    auto load_b = [&](int j, uint4 (&r)[BV]) {
+        const int c = c_lo + j / KT, tap = j - (j / KT) * KT;
+        const bool ok = j < nsteps && c * BK + q * 8 < a.cin;
 #pragma unroll
-            for (int v = 0; v < BV; ++v)
-                r[v] = bload(wr, ok ? wq + (64 * v * KT * a.cin + tap * a.cin + c * BK) * 2 : kOutOfRange);
-        };
-        static_assert(SG == 1 || (KT > 1 && SG == KT), "stage grouping: one tap, or every tap of a chunk");
-        const int hrhc = a.HR * a.HC;
-        const int aslot = ((a.nslot + 15) & ~15) * PITCH;
-        uint8_t *sA = smem;
-        uint8_t *sB = smem + 2 * aslot;
-        const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
+        for (int v = 0; v < BV; ++v)
+            r[v] = bload(wr, ok ? wq + (64 * v * KT * a.cin + tap * a.cin + c * BK) * 2 : kOutOfRange);
+    };
+    static_assert(SG == 1 || (KT > 1 && SG == KT), "stage grouping: one tap, or every tap of a chunk");
+    const int hrhc = a.HR * a.HC;
+    const int aslot = ((a.nslot + 15) & ~15) * PITCH;
+    uint8_t *sA = smem;
+    uint8_t *sB = smem + 2 * aslot;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
 
-        // halo slot -> byte offset of its input pixel (kOutOfRange: zero padding / inactive patch)
-        int aoff[AU];
+    // halo slot -> byte offset of its input pixel (kOutOfRange: zero padding / inactive patch)
+    int aoff[AU];
+#pragma unroll
+    for (int u = 0; u < AU; ++u) {
+        const int slot = (tid >> 2) + 64 * u;
+        aoff[u] = kOutOfRange;
+        if (slot < a.nslot) {
+            const int p = fdiv(slot, a.f_hrhc);
+            const int r = slot - p * hrhc;
+            const int hy = fdiv(r, a.f_hc), hx = r - hy * a.HC;
+            const int img = tb.img[p];
+            if (img >= 0) {
+                const int iy = tb.oy0[p] * S - a.pad + hy * SS;
+                const int ix = tb.ox0[p] * S - a.pad + hx * SS;
+                if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
+                    aoff[u] = (((img * a.hin + iy) * a.win + ix) * a.cin + q * 8) * 2;
+            }
+        }
+    }
+    auto load_a = [&](int c, uint4 (&r)[AU]) {
+        const bool ok = c < c_hi && c * BK + q * 8 < a.cin;
+#pragma unroll
+        for (int u = 0; u < AU; ++u)
+            r[u] = bload(xr, (ok && aoff[u] != kOutOfRange) ? aoff[u] + c * BK * 2 : kOutOfRange);
+    };
+    auto store_a = [&](uint8_t *sa, const uint4 (&r)[AU]) {
 #pragma unroll
         for (int u = 0; u < AU; ++u) {
             const int slot = (tid >> 2) + 64 * u;
-            aoff[u] = kOutOfRange;
-            if (slot < a.nslot) {
-                const int p = fdiv(slot, a.f_hrhc);
-                const int r = slot - p * hrhc;
-                const int hy = fdiv(r, a.f_hc), hx = r - hy * a.HC;
-                const int img = tb.img[p];
-                if (img >= 0) {
-                    const int iy = tb.oy0[p] * S - a.pad + hy * SS;
-                    const int ix = tb.ox0[p] * S - a.pad + hx * SS;
-                    if (iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win)
-                        aoff[u] = (((img * a.hin + iy) * a.win + ix) * a.cin + q * 8) * 2;
-                }
-            }
+            if (slot < a.nslot) *(uint4 *)(sa + slot * PITCH + q * 16) = r[u];
         }
-        auto load_a = [&](int c, uint4 (&r)[AU]) {
-            const bool ok = c < c_hi && c * BK + q * 8 < a.cin;
+    };
+    auto store_b = [&](uint8_t *sb, const uint4 (&r)[BV]) {
 #pragma unroll
-            for (int u = 0; u < AU; ++u)
-                r[u] = bload(xr, (ok && aoff[u] != kOutOfRange) ? aoff[u] + c * BK * 2 : kOutOfRange);
-        };
-        auto store_a = [&](uint8_t *sa, const uint4 (&r)[AU]) {
+        for (int v = 0; v < BV; ++v) *(uint4 *)(sb + ((tid >> 2) + 64 * v) * PITCH + q * 16) = r[v];
+    };
+    int abase[MI];
+    const int rbw = a.R * a.bw;
 #pragma unroll
-            for (int u = 0; u < AU; ++u) {
-                const int slot = (tid >> 2) + 64 * u;
-                if (slot < a.nslot) *(uint4 *)(sa + slot * PITCH + q * 16) = r[u];
-            }
-        };
-        auto store_b = [&](uint8_t *sb, const uint4 (&r)[BV]) {
-#pragma unroll
-            for (int v = 0; v < BV; ++v) *(uint4 *)(sb + ((tid >> 2) + 64 * v) * PITCH + q * 16) = r[v];
-        };
-        int abase[MI];
-        const int rbw = a.R * a.bw;
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi) {
-            const int m = wm * WM + mi * 16 + (lane & 15);
-            const int p = fdiv(m, a.f_rbw);
-            const int local = m - p * rbw;
-            const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
-            abase[mi] = (p * hrhc + pr * ST * a.HC + pc * ST) * PITCH + (lane >> 4) * 16;
-        }
-        const int boff = (wn * WN + (lane & 15)) * PITCH + (lane >> 4) * 16;
+    for (int mi = 0; mi < MI; ++mi) {
+        const int m = wm * WM + mi * 16 + (lane & 15);
+        const int p = fdiv(m, a.f_rbw);
+        const int local = m - p * rbw;
+        const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
+        abase[mi] = (p * hrhc + pr * ST * a.HC + pc * ST) * PITCH + (lane >> 4) * 16;
+    }
+    const int boff = (wn * WN + (lane & 15)) * PITCH + (lane >> 4) * 16;
 
-        f32x4 acc[MI][NI];
+    f32x4 acc[MI][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](const uint8_t *sa, const uint8_t *sb, int toff) {
+        short8 af[MI], bf[NI];
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi) af[mi] = *(const short8 *)(sa + abase[mi] + toff);
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni) bf[ni] = *(const short8 *)(sb + boff + ni * 16 * PITCH);
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-        auto compute = [&](const uint8_t *sa, const uint8_t *sb, int toff) {
-            short8 af[MI], bf[NI];
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi) af[mi] = *(const short8 *)(sa + abase[mi] + toff);
-#pragma unroll
-            for (int ni = 0; ni < NI; ++ni) bf[ni] = *(const short8 *)(sb + boff + ni * 16 * PITCH);
-#pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
-        };
-
-        Epilogue<BF16, BM, BN> epi;
-        if constexpr (KT == 1) {
-            // every k step is a new chunk: halo and weights ride D-deep register rings
-            constexpr int D = 4;
-            uint4 ra[D][AU];
-            uint4 rb[D][BV];
-#pragma unroll
-            for (int d = 0; d < D; ++d) {
-                load_a(c_lo + d, ra[d]);
-                load_b(d, rb[d]);
-            }
-            epi.prefetch(a, tb, n0);
-            auto step = [&](auto dc, int j) {
-                constexpr int d = decltype(dc)::value;
-                uint8_t *sa = sA + (j & 1) * aslot;
-                uint8_t *sb = sB + (j & 1) * BN * PITCH;
-                store_a(sa, ra[d]);
-                store_b(sb, rb[d]);
-                __syncthreads();
-                load_b(j + D, rb[d]);
-                load_a(c_lo + j + D, ra[d]);
-                compute(sa, sb, 0);
-            };
-            ring_loop<D>(step, nsteps);
-        } else if constexpr (SG == 1) {
-            // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
-            // while the current chunk is multiplied
-            uint4 ra[AU];
-            uint4 rb[KT][BV];
-            load_a(c_lo, ra);
-#pragma unroll
-            for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
-            epi.prefetch(a, tb, n0);
-            const int nch = c_hi - c_lo;
-            for (int cj = 0; cj < nch; ++cj) {
-                uint8_t *sa = sA + (cj & 1) * aslot;
-                store_a(sa, ra);
-#pragma unroll
-                for (int t = 0; t < KT; ++t) {
-                    const int j = cj * KT + t;
-                    uint8_t *sb = sB + (j & 1) * BN * PITCH;
-                    store_b(sb, rb[t]);
-                    __syncthreads();
-                    load_b(j + KT, rb[t]);
-                    if (t == 0) load_a(c_lo + cj + 1, ra);
-                    compute(sa, sb, ((t / KS) * a.HC + (t % KS)) * PITCH);
-                }
-            }
-        } else {
-            // a stage is one chunk with every tap: its halo and all KT weight slices are
-            // staged under one barrier; chunks ride a 2-deep register ring and an LDS double
-            // buffer (sB holds KT slices per buffer)
-            constexpr int D = 2;
-            const int nch = c_hi - c_lo;
-            uint4 ra[D][AU];
-            uint4 rb[D][KT][BV];
-            auto load_stage = [&](int cj, uint4 (&xa)[AU], uint4 (&xb)[KT][BV]) {
-                load_a(c_lo + cj, xa);
-#pragma unroll
-                for (int t = 0; t < KT; ++t) load_b(cj * KT + t, xb[t]);
-            };
-#pragma unroll
-            for (int d = 0; d < D; ++d) load_stage(d, ra[d], rb[d]);
-            epi.prefetch(a, tb, n0);
-            auto step = [&](auto dc, int cj) {
-                constexpr int d = decltype(dc)::value;
-                uint8_t *sa = sA + (cj & 1) * aslot;
-                uint8_t *sb = sB + (cj & 1) * KT * BN * PITCH;
-                store_a(sa, ra[d]);
-#pragma unroll
-                for (int t = 0; t < KT; ++t) store_b(sb + t * BN * PITCH, rb[d][t]);
-                __syncthreads();
-                load_stage(cj + D, ra[d], rb[d]);
-#pragma unroll
-                for (int t = 0; t < KT; ++t)
-                    compute(sa, sb + t * BN * PITCH, ((t / KS) * a.HC + (t % KS)) * PITCH);
-            };
-            ring_loop<D>(step, nch);
-        }
-
-        if constexpr (BM == 64 && BN == 64)
-            if (a.ksplit > 1 && !split_k_handoff(a, acc, mt * a.ntn + nt, ks, &s_last)) return true;
-        epi.finish(a, acc, smem, n0);
-        return true;
+            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
     };
-    if constexpr (PERSIST) {
-        // persistent (layers whose full-frame grid is much larger than what is resident):
-        // the host caps the grid at the resident workgroups and each walks L = blockIdx.x,
-        // + gridDim.x, ... until the first tile beyond the active count, so workgroups of
-        // inactive tiles are never dispatched
-        for (int L = blockIdx.x; L < a.tiles_full; L += gridDim.x) {
-            __syncthreads();                      // the previous tile's LDS use is done
-            if (!run_tile(L)) break;
+
+    Epilogue<BF16, BM, BN> epi;
+    if constexpr (KT == 1) {
+        // every k step is a new chunk: halo and weights ride D-deep register rings
+        constexpr int D = 4;
+        uint4 ra[D][AU];
+        uint4 rb[D][BV];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            load_a(c_lo + d, ra[d]);
+            load_b(d, rb[d]);
+        }
+        epi.prefetch(a, tb, n0);
+        auto step = [&](auto dc, int j) {
+            constexpr int d = decltype(dc)::value;
+            uint8_t *sa = sA + (j & 1) * aslot;
+            uint8_t *sb = sB + (j & 1) * BN * PITCH;
+            store_a(sa, ra[d]);
+            store_b(sb, rb[d]);
+            __syncthreads();
+            load_b(j + D, rb[d]);
+            load_a(c_lo + j + D, ra[d]);
+            compute(sa, sb, 0);
+        };
+        ring_loop<D>(step, nsteps);
+    } else if constexpr (SG == 1) {
+        // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
+        // while the current chunk is multiplied
+        uint4 ra[AU];
+        uint4 rb[KT][BV];
+        load_a(c_lo, ra);
+#pragma unroll
+        for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
+        epi.prefetch(a, tb, n0);
+        const int nch = c_hi - c_lo;
+        for (int cj = 0; cj < nch; ++cj) {
+            uint8_t *sa = sA + (cj & 1) * aslot;
+            store_a(sa, ra);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) {
+                const int j = cj * KT + t;
+                uint8_t *sb = sB + (j & 1) * BN * PITCH;
+                store_b(sb, rb[t]);
+                __syncthreads();
+                load_b(j + KT, rb[t]);
+                if (t == 0) load_a(c_lo + cj + 1, ra);
+                compute(sa, sb, ((t / KS) * a.HC + (t % KS)) * PITCH);
+            }
         }
     } else {
-        run_tile(blockIdx.x);
+        // a stage is one chunk with every tap: its halo and all KT weight slices are
+        // staged under one barrier; chunks ride a 2-deep register ring and an LDS double
+        // buffer (sB holds KT slices per buffer)
+        constexpr int D = 2;
+        const int nch = c_hi - c_lo;
+        uint4 ra[D][AU];
+        uint4 rb[D][KT][BV];
+        auto load_stage = [&](int cj, uint4 (&xa)[AU], uint4 (&xb)[KT][BV]) {
+            load_a(c_lo + cj, xa);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) load_b(cj * KT + t, xb[t]);
+        };
+#pragma unroll
+        for (int d = 0; d < D; ++d) load_stage(d, ra[d], rb[d]);
+        epi.prefetch(a, tb, n0);
+        auto step = [&](auto dc, int cj) {
+            constexpr int d = decltype(dc)::value;
+            uint8_t *sa = sA + (cj & 1) * aslot;
+            uint8_t *sb = sB + (cj & 1) * KT * BN * PITCH;
+            store_a(sa, ra[d]);
+#pragma unroll
+            for (int t = 0; t < KT; ++t) store_b(sb + t * BN * PITCH, rb[d][t]);
+            __syncthreads();
+            load_stage(cj + D, ra[d], rb[d]);
+#pragma unroll
+            for (int t = 0; t < KT; ++t)
+                compute(sa, sb + t * BN * PITCH, ((t / KS) * a.HC + (t % KS)) * PITCH);
+        };
+        ring_loop<D>(step, nch);
     }
+
+    if constexpr (BM == 64 && BN == 64)
+        if (a.ksplit > 1 && !split_k_handoff(a, acc, mt * a.ntn + nt, ks, &s_last)) return;
+    epi.finish(a, acc, smem, n0);
 }
 
 // ------------------------------------------------------------------ stem form
@@ -931,7 +915,6 @@ struct Plan {
     Form form;
     MfmaArgs a;
     int sg = 1;                // pipelined form: stage grouping (k_conv_pipe's SG)
-    bool persist = false;      // pipelined form: persistent tile walk (k_conv_pipe's PERSIST)
     unsigned tiles;            // output tiles of a full frame (before any K split)
     size_t lds;
     size_t ws_bytes;
@@ -1029,7 +1012,8 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 // and K split over every ResNet-50 layer of a 2048x1024 frame with 30 % of the blocks
 // active: 64-row tiles are fastest everywhere (at these sizes the kernel is bound by
 // latency and occupancy, and 64x64 tiles keep the most workgroups resident); 128-wide N
-// tiles pay off only for 1x1 layers with 64 input channels; splitting K in two pays off
+// tiles pay off for 1x1 layers with blocks of 256 or more pixels (the stride-4 and
+// stride-8 maps, many tiles per block) and Cout a multiple of 128; splitting K in two pays off
 // when a full frame has at most 256 tiles (the stride-32 layers) and for 3x3 layers
 // with 512 or more input channels and 513 to 2048 tiles (where nine-tap stages do not
 // apply).
@@ -1039,7 +1023,7 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 bool choose_plan(const LayerGeom &g, Plan &best)
 {
     if ((g.kh == 1 || g.kh == 3) && g.cin % 8 == 0) {
-        const int bn = (g.kh == 1 && g.cin <= 64 && g.cout >= 256 && g.cout % 128 == 0) ? 128 : 64;
+        const int bn = (g.kh == 1 && g.cout % 128 == 0 && g.bh * g.bw >= 256) ? 128 : 64;
         if (make_plan(g, 64, bn, best) || make_plan(g, 64, 64, best)) {
             MfmaArgs &a = best.a;
             const int nchunk = (g.cin + BK - 1) / BK;
@@ -1067,11 +1051,6 @@ bool choose_plan(const LayerGeom &g, Plan &best)
                     best.lds = lds;
                 }
             }
-            // 1x1 layers with a full-frame grid of 4096 or more workgroups (the stride-4
-            // and stride-8 layers with 256 or more output channels) walk their tiles
-            // persistently: dispatching and retiring the inactive tiles' workgroups costs
-            // more there than the walk's extra registers
-            best.persist = g.kh == 1 && best.BM == 64 && best.grid >= 4096;
             best.a.tiles_full = (int)best.grid;
             return true;
         }
@@ -1126,8 +1105,6 @@ hipError_t workspace(size_t bytes, float **out)
 
 std::mutex g_attr_mu;
 std::map<const void *, size_t> g_attr_lds;   // dynamic LDS each kernel has opted in to
-// resident workgroups of a device for (kernel, dynamic LDS), per device ordinal
-std::map<std::pair<const void *, size_t>, std::array<int, 64>> g_resident;
 
 template <typename K>
 hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
@@ -1144,27 +1121,7 @@ hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
             cur = p.lds;
         }
     }
-    unsigned grid = p.grid;
-    if (p.form == Form::Pipe && p.persist) {
-        // persistent kernel: as many workgroups as are resident at once (at most the
-        // tiles of a full frame), cached per kernel, LDS size and device
-        int dev = 0;
-        hipError_t e = hipGetDevice(&dev);
-        if (e != hipSuccess) return e;
-        if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-        std::lock_guard<std::mutex> lk(g_attr_mu);
-        int &cap = g_resident[std::make_pair((const void *)kernel, p.lds)][dev];
-        if (cap == 0) {
-            int cus = 0, per_cu = 0;
-            e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-            if (e != hipSuccess) return e;
-            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, p.lds);
-            if (e != hipSuccess) return e;
-            cap = (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
-        }
-        if (grid > (unsigned)cap) grid = (unsigned)cap;
-    }
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), p.lds, s, p.a);
+    hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads), p.lds, s, p.a);
     return hipSuccess;
 }
 
@@ -1178,14 +1135,10 @@ hipError_t launch_one(const Plan &p, hipStream_t s)
         }
     } else if (p.form == Form::Pipe) {
         if constexpr (KS == 1 || KS == 3) {
-            // all-tap stages exist for the 64x64 tiles the planner gives them to, the
-            // persistent walk for 64-row 1x1 tiles
-            if constexpr (BM == 64 && BN == 64 && KS == 3)
-                if (p.sg == 9) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 9, false>, p, s);
-            if constexpr (BM == 64 && KS == 1)
-                if (p.persist) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 1, true>, p, s);
-            if (p.sg == 1 && !p.persist)
-                return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 1, false>, p, s);
+            // all-tap stages exist for the 64x64 tiles the planner gives them to
+                if constexpr (BM == 64 && BN == 64 && KS == 3)
+                if (p.sg == 9) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 9>, p, s);
+            if (p.sg == 1) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 1>, p, s);
         }
     } else {
         return launch_kernel(k_conv_mfma<BF16, BM, BN, KS, S>, p, s);
