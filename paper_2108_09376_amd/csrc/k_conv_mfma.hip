@@ -819,37 +819,72 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
         (void *)a.w, (short)0, a.w_bytes, kBufferFlags);
     const int wbase = n0 * KS * kwc * 2;
     const int nvec = (wvals * 2 + 15) / 16;
-    for (int v = tid; v < nvec; v += kThreads)
-        *(uint4 *)((uint8_t *)sW + v * 16) = bload(wr, wbase + v * 16);
+    // every thread's requests (halo values, then raw weights) are issued before any of
+    // them is used, so the staging costs one memory round trip instead of one per item
+    constexpr int WPT = 6;                   // 16-byte weight vectors per thread per batch
+    constexpr int SPT = 6;                   // halo pixels per thread per batch
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
+    const int npix = a.P * a.HR * hcp;
+    auto halo_batch = [&](int e0, uint16_t (&v)[SPT][CP]) {
+#pragma unroll
+        for (int u = 0; u < SPT; ++u) {
+            const int e = e0 + u * kThreads + tid;
+            const int row = fdiv(e, a.f_hc);                  // f_hc holds 1 / hcp here
+            const int col = e - row * hcp;
+            const int p = min(fdiv(row, a.f_hrhc), a.P - 1);  // f_hrhc holds 1 / HR here
+            const int hy = row - p * a.HR;
+            const int img = tb.img[p];
+            const int iy = tb.oy0[p] * S - a.pad + hy, ix = tb.ox0[p] * S - a.pad + col;
+            int off = (e < npix && img >= 0 && col < a.HC && iy >= 0 && iy < a.hin && ix >= 0 &&
+                       ix < a.win)
+                          ? (((img * a.hin + iy) * a.win + ix) * a.cin) * 2
+                          : kOutOfRange;
+            asm volatile("" : "+v"(off));
+#pragma unroll
+            for (int c = 0; c < CP; ++c)
+                v[u][c] = c < a.cin ? __builtin_amdgcn_raw_buffer_load_b16(xr, off + 2 * c, 0, 0)
+                                    : (uint16_t)0;
+        }
+    };
+    auto halo_store = [&](int e0, const uint16_t (&v)[SPT][CP]) {
+#pragma unroll
+        for (int u = 0; u < SPT; ++u) {
+            const int e = e0 + u * kThreads + tid;
+            if (e >= npix) continue;
+            if constexpr (CP == 4) {
+                *(uint2 *)(sA + (size_t)e * 8) = make_uint2(v[u][0] | ((uint32_t)v[u][1] << 16),
+                                                            v[u][2] | ((uint32_t)v[u][3] << 16));
+            } else {
+                *(uint4 *)(sA + (size_t)e * 16) = make_uint4(
+                    v[u][0] | ((uint32_t)v[u][1] << 16), v[u][2] | ((uint32_t)v[u][3] << 16),
+                    v[u][4] | ((uint32_t)v[u][5] << 16), v[u][6] | ((uint32_t)v[u][7] << 16));
+            }
+        }
+    };
+    uint16_t hv[SPT][CP];
+    halo_batch(0, hv);
+    for (int v0 = 0; v0 < nvec; v0 += WPT * kThreads) {
+        uint4 wv[WPT];
+#pragma unroll
+        for (int u = 0; u < WPT; ++u) {
+            const int v = v0 + u * kThreads + tid;
+            wv[u] = bload(wr, v < nvec ? wbase + v * 16 : kOutOfRange);
+        }
+#pragma unroll
+        for (int u = 0; u < WPT; ++u) {
+            const int v = v0 + u * kThreads + tid;
+            if (v < nvec) *(uint4 *)((uint8_t *)sW + v * 16) = wv[u];
+        }
+    }
     Epilogue<BF16, BM, BN> epi;
     epi.prefetch(a, tb, n0);
 
     // halo pixels with CP channels each (zeros outside the image, past Cin, in the tail)
-    const int npix = a.P * a.HR * hcp;
-    for (int e = tid; e < npix; e += kThreads) {
-        const int row = fdiv(e, a.f_hc);                  // f_hc holds 1 / hcp here
-        const int col = e - row * hcp;
-        const int p = fdiv(row, a.f_hrhc);               // f_hrhc holds 1 / HR here
-        const int hy = row - p * a.HR;
-        uint16_t v[CP];
-#pragma unroll
-        for (int c = 0; c < CP; ++c) v[c] = 0;
-        const int img = tb.img[p];
-        const int iy = tb.oy0[p] * S - a.pad + hy, ix = tb.ox0[p] * S - a.pad + col;
-        if (img >= 0 && col < a.HC && iy >= 0 && iy < a.hin && ix >= 0 && ix < a.win) {
-            const uint16_t *src = a.x + (((size_t)img * a.hin + iy) * a.win + ix) * a.cin;
-#pragma unroll
-            for (int c = 0; c < CP; ++c)
-                if (c < a.cin) v[c] = src[c];
-        }
-        if constexpr (CP == 4) {
-            *(uint2 *)(sA + (size_t)e * 8) = make_uint2(v[0] | ((uint32_t)v[1] << 16),
-                                                        v[2] | ((uint32_t)v[3] << 16));
-        } else {
-            *(uint4 *)(sA + (size_t)e * 16) = make_uint4(
-                v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-        }
+    halo_store(0, hv);
+    for (int e0 = SPT * kThreads; e0 < npix; e0 += SPT * kThreads) {
+        halo_batch(e0, hv);
+        halo_store(e0, hv);
     }
     __syncthreads();
     // rearrange weights: B[i][n][kk] = W[n][i][j][c] with kk = j*CP + c, zero elsewhere
