@@ -449,28 +449,33 @@ __device__ uint32_t g_split_counter[kMaxSplitTiles];   // zero at load, reset af
 // Split-K hand-off: every K slice of a tile stores its fp32 partial (the four waves'
 // MI x NI fragments), and the last slice to arrive (per-tile counter) adds all
 // partials in slice order 0, 1, ... into `acc` and returns true; the others return
-// false and exit. Partials are written through to the device-coherent level
-// (agent-scope atomic stores), all of this workgroup's stores are waited for before
-// the counter is incremented, and the last slice reads the others' partials with
-// agent-scope loads, so no cache-wide write-back or invalidate is needed. The last
-// slice resets the counter, so no memset is needed between calls (safe under graph
-// replay).
+// false and exit. A fragment's four values per lane are one 16-byte access and a
+// wave's 64 lanes one contiguous kilobyte. Partials are written through to the
+// device-coherent level (the SC1 cache policy of agent-scope atomic stores), all of
+// this workgroup's stores are waited for before the per-tile counter is incremented,
+// and the last slice reads the others' partials with the same policy, so no cache-wide
+// write-back or invalidate is needed. The last slice resets the counter, so no memset
+// is needed between calls (safe under graph replay).
+constexpr int kCoherentSC1 = 16;            // cache policy: SC1 (device-coherent access)
+
 template <int MI, int NI>
 __device__ __forceinline__ bool split_k_handoff(const MfmaArgs &a, f32x4 (&acc)[MI][NI], int tile,
                                                 int ks, int *s_last)
 {
     constexpr int SLICE = 4 * MI * NI * 64 * 4;     // floats of one slice's partial tile
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    float *base = a.ws + (size_t)tile * a.ksplit * SLICE;
-    float *mine = base + (size_t)ks * SLICE;
+    const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.ws + (size_t)tile * a.ksplit * SLICE), (short)0, a.ksplit * SLICE * 4,
+        kBufferFlags);
+    auto frag_off = [&](int sl, int mi, int ni) {
+        return (sl * SLICE + (((wave * MI + mi) * NI + ni) * 64 + lane) * 4) * 4;
+    };
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                __hip_atomic_store(mine + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4 + i,
-                                   acc[mi][ni][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[mi][ni]), pr,
+                                                   frag_off(ks, mi, ni), 0, kCoherentSC1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0)
@@ -483,16 +488,13 @@ __device__ __forceinline__ bool split_k_handoff(const MfmaArgs &a, f32x4 (&acc)[
 #pragma unroll
     for (int sl = 0; sl < kMaxSplit; ++sl) {
         if (sl >= a.ksplit || sl == ks) continue;
-        const float *src = base + (size_t)sl * SLICE;
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-                const float *e = src + ((size_t)((wave * MI + mi) * NI + ni) * 64 + lane) * 4;
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    part[sl][mi][ni][i] = __hip_atomic_load(e + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+            for (int ni = 0; ni < NI; ++ni)
+                part[sl][mi][ni] = __builtin_bit_cast(
+                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(pr, frag_off(sl, mi, ni), 0,
+                                                                 kCoherentSC1));
     }
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)

@@ -214,7 +214,9 @@ FULL = [
     (512, 512, 64, 128, 8, 16, 3, 2, False),     # stride-2 3x3, 4x4 output blocks
     (1024, 2048, 64, 128, 8, 16, 1, 2, False),   # stride-2 1x1 downsample
     (64, 256, 256, 512, 8, 16, 1, 1, True),      # 4096 full-frame tiles: persistent tile walk
-    (128, 512, 256, 512, 8, 16, 1, 2, False),    # stride-2 1x1 with 4096 tiles: persistent
+    (128, 512, 256, 512, 8, 16, 1, 2, False),    # stride-2 1x1 with 4096 full-frame tiles
+    (512, 512, 32, 64, 8, 16, 3, 1, False),      # stride-32 3x3: K split over two workgroups
+    (2048, 512, 32, 64, 8, 16, 1, 1, False),     # stride-32 1x1: K split over two workgroups
 ]
 
 
