@@ -98,6 +98,51 @@ def swiftnet_table(depth: int = 18, classes: int = 19, width: int = 128):
     return L
 
 
+def policy_table():
+    """The policy network (Section 3.3; reading in policy.py): on S_t (32 channels at a
+    quarter of the frame resolution) a 3x3 stride-2 stem to 64 channels, three basic
+    residual blocks (64, 128, 256 channels; the second and third stride 2 with a 1x1
+    stride-2 projection on the shortcut), then a fully convolutional head of two 3x3
+    stride-2 convolutions down to one pixel per 128-pixel block (64 channels, channel 0
+    is the block's logit, no ReLU on the last)."""
+    L = []
+
+    def conv(name, src, cin, cout, k, s, relu, res=None):
+        L.append(dict(kind="conv", name=name, src=src, res=res, cin=cin, cout=cout,
+                      k=k, stride=s, pad=k // 2, relu=relu))
+        return len(L) - 1
+
+    x = conv("pn.stem", -1, 32, 64, 3, 2, True)
+    a = conv("pn.block1.conv1", x, 64, 64, 3, 1, True)
+    x = conv("pn.block1.conv2", a, 64, 64, 3, 1, True, res=x)
+    cin = 64
+    for i, c in ((2, 128), (3, 256)):
+        ds = conv(f"pn.block{i}.downsample", x, cin, c, 1, 2, False)
+        a = conv(f"pn.block{i}.conv1", x, cin, c, 3, 2, True)
+        x = conv(f"pn.block{i}.conv2", a, c, c, 3, 1, True, res=ds)
+        cin = c
+    x = conv("pn.head1", x, 256, 64, 3, 2, True)
+    conv("pn.head2", x, 64, 64, 3, 2, False)
+    return L
+
+
+def dense_frame(table, folded, x_bits, dtype):
+    """Every layer on every pixel (a full execution grid)."""
+    n = x_bits.shape[0]
+    ones = np.ones((n, 1, 1), np.uint8)
+    out = []
+    for li, l in enumerate(table):
+        src = x_bits if l["src"] < 0 else out[l["src"]]
+        res = None if l["res"] is None else out[l["res"]]
+        oh = (src.shape[2] + 2 * l["pad"] - l["k"]) // l["stride"] + 1
+        ow = (src.shape[3] + 2 * l["pad"] - l["k"]) // l["stride"] + 1
+        prev = np.zeros((n, l["cout"], oh, ow), np.uint16)
+        out.append(sparse_conv2d(src, folded[li]["w_bits"], ones, prev, dtype, stride=l["stride"],
+                                 pad=l["pad"], bias=folded[li]["bias"], residual_bits=res,
+                                 relu=l["relu"]))
+    return out
+
+
 def make_params(table, seed0=1000, bn_random=False):
     """Per-conv fp32 OIHW weights (He-normal, seed seed0 + layer index) and BN
     parameters. Random init uses gamma=1, beta=0, mean=0, var=1 unless bn_random."""

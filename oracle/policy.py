@@ -22,6 +22,14 @@ excepted, see below), written from the paper's definitions:
   divergence between the output distributions of frame t and frame t-1; per block, the
   maximum over its pixels (Eq. 1). Readings: the direction is KL(O_t || O_{t-1});
   the network hands over per-class scores (logits) and O = softmax over classes.
+* Section 3.3 and Eq. 2: the policy network maps S_t = {I_t, H_{t-1}, A_{t-1}, O_{t-1}}
+  to one execution probability per block. The architecture is given only as a figure
+  (an 8-layer ResNet backbone with a fully convolutional head, about 6.5 GMACs on a
+  2048x1024 frame, the extra inputs adding about 0.1 GMAC). Reading: S_t is assembled
+  at a quarter of the frame resolution, where O_{t-1} lives, as 32 channels (the
+  frame and the frame state averaged over 4x4 pixels, the class probabilities of
+  O_{t-1}, A_{t-1} of the pixel's block, zeros); the network ends in a map with one
+  pixel per block whose channel 0 is the block's logit, p_b = sigmoid(logit).
 * Section 3.5: rewards. R_IG = IG_b if a_b = 1, else -IG_b. C_t = fraction of executed
   blocks of the frame. M_t = (1 - mu) C_t + mu M_{t-1}, reading the printed C_{t-1} as
   the previous moving average M_{t-1} (the text calls M a moving average with
@@ -157,3 +165,40 @@ def reinforce_loss(reward, mask, prob):
     with np.errstate(divide="ignore"):
         logpi = np.where(a, np.log(p), np.log1p(-p))
     return -(r * logpi).reshape(r.shape[0], -1).sum(axis=1)
+
+
+POLICY_CHANNELS = 32       # channels of S_t
+
+
+def policy_input(frame_bits, state_bits, score_bits, classes: int, prev_mask, dtype="bf16"):
+    """S_t at a quarter of the frame resolution, as storage bits [n, 32, h/4, w/4].
+
+    frame_bits, state_bits: I_t and H_{t-1}, [n, 3, h, w] bits; score_bits: O_{t-1}'s
+    per-class scores [n, C, h/4, w/4] bits (the first `classes` channels are used);
+    prev_mask: A_{t-1}, uint8 [n, gh, gw] over the frame's block grid, or None (zeros).
+    Channels: 0-2 the mean of I_t over each 4x4 pixel cell, 3-5 the same for H_{t-1},
+    6 .. 5+classes the softmax over classes of O_{t-1} (its output probabilities),
+    6+classes: a_b of the block the pixel lies in, the rest 0. Values in float64,
+    stored once (fp64 -> fp32 -> storage format, round to nearest even)."""
+    from . import store, value
+    f = value(frame_bits, dtype)
+    st = value(state_bits, dtype)
+    n, _, h, w = f.shape
+    h4, w4 = h // 4, w // 4
+    z = np.zeros((n, POLICY_CHANNELS, h4, w4))
+    z[:, 0:3] = f.reshape(n, 3, h4, 4, w4, 4).mean(axis=(3, 5))
+    z[:, 3:6] = st.reshape(n, 3, h4, 4, w4, 4).mean(axis=(3, 5))
+    sc = value(score_bits, dtype)[:, :classes]
+    z[:, 6:6 + classes] = np.exp(log_softmax(sc, axis=1))
+    if prev_mask is not None:
+        m = np.asarray(prev_mask) != 0
+        gh, gw = m.shape[1:]
+        z[:, 6 + classes] = np.repeat(np.repeat(m, h4 // gh, axis=1), w4 // gw, axis=2)
+    return store(z, dtype)
+
+
+def policy_probabilities(logit_bits, dtype="bf16"):
+    """p_b = sigmoid(channel 0) of the head's [n, C, gh, gw] output. float64 [n, gh, gw]."""
+    from . import value
+    v = value(logit_bits, dtype)[:, 0]
+    return 1.0 / (1.0 + np.exp(-v))
