@@ -245,7 +245,10 @@ def policy_steps(torch, bc, dev):
       upsample_add      the decoder's largest merge (128x256 -> 256x512, 128 channels,
                         bf16, skip added, 38 blocks); algorithmic bytes = the active
                         blocks' coarse tiles with their one-pixel halo and skip read
-                        once, the output blocks written once"""
+                        once, the output blocks written once
+      policy_forward    the policy network on a 2048x1024 frame (random init): S_t
+                        assembly, eleven dense convolutions, the block probabilities;
+                        FLOPs = 2 x its MACs"""
     import numpy as np
 
     import synth
@@ -287,6 +290,10 @@ def policy_steps(torch, bc, dev):
                                                            idx38, cnt38),
                          38 * 128 * 2 * ((16 + 2) * (16 + 2) + 2 * 32 * 32)),
     }
+    from paper_2108_09376_amd import resnet
+    pnet = resnet.PolicyNet(1024, 2048, device=dev)
+    scores = torch.randn((1, 256, 512, 64), device=dev).to(torch.bfloat16)
+    ops["policy_forward"] = (lambda: pnet.forward(frame, state, scores, mask), None)
     out = {}
     for name, (fn, nbytes) in ops.items():
         fn()
@@ -308,6 +315,9 @@ def policy_steps(torch, bc, dev):
         if nbytes:
             row.update({"bytes": nbytes, "GBps": round(nbytes / us / 1e3, 1),
                         "frac_of_hbm_peak": round(nbytes / us / 1e3 / PEAK_HBM_GBS, 3)})
+        if name == "policy_forward":
+            row.update({"gmac": round(pnet.macs() / 1e9, 3),
+                        "tflops": round(2 * pnet.macs() / us / 1e6, 1)})
         out[name] = row
         del g
     return out

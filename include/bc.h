@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 3
+#define BC_ABI_VERSION 4
 
 typedef enum {
     BC_OK = 0,
@@ -306,6 +306,39 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
  */
 bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logits,
                                   bc_tensor desc, int32_t classes, bc_grid g, float *d_ig,
+                                  void *stream);
+
+/*
+ * Input of the policy network (Section 3.3, Eq. 2: S_t = {I_t, H_{t-1}, A_{t-1},
+ * O_{t-1}}), assembled at a quarter of the frame resolution, where the segmentation
+ * output lives, as 32 channels per pixel:
+ *   0-2   I_t averaged over the pixel's 4x4 cell of the frame,
+ *   3-5   H_{t-1} (the frame state) averaged the same way,
+ *   6 .. 5+classes   softmax over the first `classes` channels of O_{t-1}'s scores,
+ *   6+classes        a_b of A_{t-1} for the block the pixel lies in (0 if NULL),
+ *   the rest 0.
+ * Arithmetic fp32, one round-to-nearest-even to the storage dtype.
+ *   d_frame, d_state  [n][h][w][3] NHWC, BF16 or F16, h and w multiples of 4, < 2 GiB.
+ *   d_scores          [n][h/4][w/4][c] NHWC, same dtype, c % 8 == 0, 1 <= classes <= min(c, 24).
+ *   d_prev_mask       uint8 [n][grid_h][grid_w] or NULL; the grid divides h/4 x w/4.
+ *   d_out             [n][h/4][w/4][32] NHWC, same dtype, written completely.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE,
+ * BC_ERR_ALIAS (d_out overlapping an input), BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ */
+bc_status bc_policy_input(const void *d_frame, const void *d_state, bc_tensor frame,
+                          const void *d_scores, bc_tensor scores, int32_t classes,
+                          const uint8_t *d_prev_mask, bc_grid g, void *d_out, bc_tensor out,
+                          void *stream);
+
+/*
+ * Block probabilities P_t of the policy network (Section 3.5: p_b in [0, 1] per block):
+ * p_b = 1 / (1 + exp(-logit_b)), logit_b = channel 0 of the head's output map, which
+ * has one pixel per block.
+ *   d_logits  [n][grid_h][grid_w][c] NHWC, BF16 or F16 (desc.h, desc.w = the grid).
+ *   d_prob    float32 [n][grid_h][grid_w], device, written.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS, BC_ERR_HIP.
+ */
+bc_status bc_policy_probabilities(const void *d_logits, bc_tensor logits, float *d_prob,
                                   void *stream);
 
 /*

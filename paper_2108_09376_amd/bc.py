@@ -74,6 +74,8 @@ _sigs = {
     "bc_sparse_upsample_add": ([_vp, bc_tensor, _vp, _vp, bc_tensor, bc_grid, _i32, _vp, _vp, _i32,
                                 _vp], _i32),
     "bc_seg_information_gain": ([_vp, _vp, bc_tensor, _i32, bc_grid, _vp, _vp], _i32),
+    "bc_policy_input": ([_vp, _vp, bc_tensor, _vp, bc_tensor, _i32, _vp, bc_grid, _vp, bc_tensor, _vp], _i32),
+    "bc_policy_probabilities": ([_vp, bc_tensor, _vp, _vp], _i32),
     "bc_block_rewards": ([_vp, _vp, _vp, _i32, bc_grid, _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
@@ -85,7 +87,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 3
+ABI_VERSION = 4
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -251,6 +253,21 @@ def bc_seg_information_gain(logits, prev_logits, grid, ig, classes=None, layout=
                                       int(d.c if classes is None else classes), _grid(grid),
                                       _ptr(ig), _stream(stream))
     _check(st, "bc_seg_information_gain")
+
+
+def bc_policy_input(frame, state, scores, classes, prev_mask, grid, out, stream=None):
+    """S_t [n, h/4, w/4, 32] (NHWC) from the frame and frame state [n, h, w, 3], the
+    previous scores [n, h/4, w/4, c] and the previous grid (uint8 [n, gh, gw] or None)."""
+    st = _lib.bc_policy_input(_ptr(frame), _ptr(state), desc(frame, BC_NHWC), _ptr(scores),
+                              desc(scores, BC_NHWC), int(classes), _ptr(prev_mask), _grid(grid),
+                              _ptr(out), desc(out, BC_NHWC), _stream(stream))
+    _check(st, "bc_policy_input")
+
+
+def bc_policy_probabilities(logits, prob, stream=None):
+    """prob float32 [n, gh, gw] = sigmoid(logits[..., 0]), logits [n, gh, gw, c] NHWC."""
+    st = _lib.bc_policy_probabilities(_ptr(logits), desc(logits, BC_NHWC), _ptr(prob), _stream(stream))
+    _check(st, "bc_policy_probabilities")
 
 
 def bc_block_rewards(ig, mask, prob, grid, tau, gamma, mu, mavg, reward, cost=None, loss=None,

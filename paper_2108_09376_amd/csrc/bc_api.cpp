@@ -630,6 +630,65 @@ bc_status bc_sparse_upsample_add(const void *d_coarse, bc_tensor coarse, const v
     return ok();
 }
 
+bc_status bc_policy_input(const void *d_frame, const void *d_state, bc_tensor frame,
+                          const void *d_scores, bc_tensor scores, int32_t classes,
+                          const uint8_t *d_prev_mask, bc_grid g, void *d_out, bc_tensor out,
+                          void *stream)
+{
+    if (!d_frame || !d_state || !d_scores || !d_out)
+        return fail(BC_ERR_NULL, "d_frame, d_state, d_scores and d_out are required");
+    bc_status st;
+    if ((st = check_tensor(frame, "frame"))) return st;
+    if ((st = check_tensor(scores, "scores"))) return st;
+    if ((st = check_tensor(out, "out"))) return st;
+    if (frame.layout != BC_NHWC || scores.layout != BC_NHWC || out.layout != BC_NHWC)
+        return fail(BC_ERR_LAYOUT, "frame, scores and out must be channels last (NHWC)");
+    if (frame.dtype == BC_F32 || scores.dtype != frame.dtype || out.dtype != frame.dtype)
+        return fail(BC_ERR_DTYPE, "frame, scores and out must share one 16-bit dtype");
+    if (frame.c != 3) return fail(BC_ERR_SHAPE, "frame must have 3 channels (got %d)", frame.c);
+    if (frame.h % 4 || frame.w % 4) return fail(BC_ERR_SHAPE, "frame size must be a multiple of 4");
+    const int h4 = frame.h / 4, w4 = frame.w / 4;
+    if (scores.n != frame.n || scores.h != h4 || scores.w != w4)
+        return fail(BC_ERR_SHAPE, "scores must be [n][h/4][w/4][c] of the frame");
+    if (scores.c % 8) return fail(BC_ERR_UNSUPPORTED, "score channels must be a multiple of 8");
+    if (classes < 1 || classes > scores.c || classes > 24)
+        return fail(BC_ERR_SHAPE, "classes %d outside 1..min(24, %d)", classes, scores.c);
+    if (out.n != frame.n || out.h != h4 || out.w != w4 || out.c != 32)
+        return fail(BC_ERR_SHAPE, "out must be [n][h/4][w/4][32]");
+    if (g.grid_h <= 0 || g.grid_w <= 0 || h4 % g.grid_h || w4 % g.grid_w)
+        return fail(BC_ERR_NOT_DIVISIBLE, "the quarter-resolution map is not divisible by the grid");
+    if (tensor_bytes(frame) >= 2147483392u)
+        return fail(BC_ERR_UNSUPPORTED, "frame must be below 2 GiB");
+    const size_t ob = tensor_bytes(out);
+    if (overlap(d_out, ob, d_frame, tensor_bytes(frame)) || overlap(d_out, ob, d_state, tensor_bytes(frame)) ||
+        overlap(d_out, ob, d_scores, tensor_bytes(scores)) ||
+        overlap(d_out, ob, d_prev_mask, (size_t)frame.n * g.grid_h * g.grid_w))
+        return fail(BC_ERR_ALIAS, "d_out overlaps an input");
+    hipError_t e = bc::launch_policy_input(d_frame, d_state, d_scores, d_prev_mask, d_out, frame.n,
+                                           frame.h, frame.w, scores.c, classes, g.grid_h, g.grid_w,
+                                           frame.dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "policy input launch");
+    return ok();
+}
+
+bc_status bc_policy_probabilities(const void *d_logits, bc_tensor logits, float *d_prob,
+                                  void *stream)
+{
+    if (!d_logits || !d_prob) return fail(BC_ERR_NULL, "d_logits and d_prob are required");
+    bc_status st = check_tensor(logits, "logits");
+    if (st) return st;
+    if (logits.layout != BC_NHWC) return fail(BC_ERR_LAYOUT, "logits must be channels last");
+    if (logits.dtype == BC_F32) return fail(BC_ERR_DTYPE, "logits must be bf16 or f16");
+    const double blocks = (double)logits.n * logits.h * logits.w;
+    if (blocks > (double)(1 << 20)) return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    if (overlap(d_prob, (size_t)blocks * 4, d_logits, tensor_bytes(logits)))
+        return fail(BC_ERR_ALIAS, "d_prob overlaps d_logits");
+    hipError_t e = bc::launch_policy_probabilities(d_logits, (int)blocks, logits.c,
+                                                   logits.dtype == BC_BF16, d_prob, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "policy probabilities launch");
+    return ok();
+}
+
 bc_status bc_block_rewards(const float *d_ig, const uint8_t *d_mask, const float *d_prob,
                            int32_t n, bc_grid g, float tau, float gamma, float mu, float *d_mavg,
                            float *d_reward, float *d_cost, float *d_loss, void *stream)

@@ -70,4 +70,12 @@ hipError_t launch_upsample_add(const void *coarse, const void *skip, void *out, 
                                int hc, int wc, int esize, bool nhwc, bool bf16, int gh, int gw,
                                const int32_t *idx, const int32_t *count, int relu, hipStream_t s);
 
+// Policy network input S_t at a quarter of the frame resolution (32 channels) and the
+// block probabilities from the head's logits (channel 0 of c).
+hipError_t launch_policy_input(const void *frame, const void *state, const void *scores,
+                               const uint8_t *mask, void *out, int n, int h, int w, int c,
+                               int classes, int gh, int gw, bool bf16, hipStream_t s);
+hipError_t launch_policy_probabilities(const void *logits, int blocks, int c, bool bf16,
+                                       float *prob, hipStream_t s);
+
 }  // namespace bc

@@ -129,6 +129,86 @@ def default_params(layers: list[Layer], seed0: int = 1000, bn_random: bool = Fal
     return out
 
 
+def device_weights(layers: list[Layer], params, dtype, device):
+    """Batch norm folded into each conv (bc_fold_bn) and the weights repacked to the
+    channels-last layout in `dtype` (bc_repack_weights), on the device; None for layers
+    without weights."""
+    dcode = bc.BC_BF16 if dtype == torch.bfloat16 else bc.BC_F16
+    weights, biases = [], []
+    for l, p in zip(layers, params):
+        if l.kind != "conv":
+            weights.append(None)
+            biases.append(None)
+            continue
+        wf, bf = bc.bc_fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
+        wr = bc.bc_repack_weights(wf.reshape(p["w"].shape), dcode)
+        weights.append(torch.from_numpy(wr.view(np.int16)).view(dtype).to(device).contiguous())
+        biases.append(torch.from_numpy(bf).to(device))
+    return weights, biases
+
+
+def build_policy_layers() -> list[Layer]:
+    """The policy network on S_t (32 channels at a quarter of the frame resolution):
+    3x3/2 stem to 64 channels, basic blocks of 64, 128 (stride 2) and 256 (stride 2)
+    channels with 1x1/2 projections on the strided shortcuts, and a fully convolutional
+    head of two 3x3/2 convolutions to one pixel per 128-pixel block (64 channels,
+    channel 0 the block's logit)."""
+    L = [Layer("conv", "pn.stem", -1, 32, 64, 3, 2)]
+    L.append(Layer("conv", "pn.block1.conv1", 0, 64, 64, 3, 1))
+    L.append(Layer("conv", "pn.block1.conv2", 1, 64, 64, 3, 1, res=0))
+    cur, ch = 2, 64
+    for i, width in ((2, 128), (3, 256)):
+        L.append(Layer("conv", f"pn.block{i}.downsample", cur, ch, width, 1, 2, relu=False))
+        ds = len(L) - 1
+        L.append(Layer("conv", f"pn.block{i}.conv1", cur, ch, width, 3, 2))
+        L.append(Layer("conv", f"pn.block{i}.conv2", len(L) - 1, width, width, 3, 1, res=ds))
+        cur, ch = len(L) - 1, width
+    L.append(Layer("conv", "pn.head1", cur, 256, 64, 3, 2))
+    L.append(Layer("conv", "pn.head2", len(L) - 1, 64, 64, 3, 2, relu=False))
+    return L
+
+
+class PolicyNet:
+    """The policy network's forward pass on the device (Section 3.3, Eq. 2): S_t
+    assembled by bc_policy_input, the convolutions on the dense path (every block; each
+    layer on a grid of at most 8x8-pixel blocks), P_t by bc_policy_probabilities.
+    h, w: frame size; block: block edge in frame pixels (the head ends on that grid)."""
+
+    def __init__(self, h: int, w: int, block: int = 128, classes: int = 19, params=None,
+                 dtype=torch.bfloat16, device="cuda", seed0: int = 3000):
+        if h % block or w % block or block != 128:
+            raise ValueError("the head reduces the frame by 128: blocks of 128 pixels")
+        self.layers = build_policy_layers()
+        self.classes, self.dtype, self.device = classes, dtype, torch.device(device)
+        self.grid = (h // block, w // block)
+        params = params if params is not None else default_params(self.layers, seed0)
+        self.shapes = layer_shapes(self.layers, h // 4, w // 4)
+        self.weights, self.biases = device_weights(self.layers, params, dtype, self.device)
+        self.input = torch.empty((1, h // 4, w // 4, 32), dtype=dtype, device=self.device)
+        self.buffers = [torch.empty((1, oh, ow, c), dtype=dtype, device=self.device)
+                        for (oh, ow, c) in self.shapes]
+        self.grids = [(oh // min(8, oh), ow // min(8, ow)) for (oh, ow, _) in self.shapes]
+        self.prob = torch.empty((1,) + self.grid, dtype=torch.float32, device=self.device)
+
+    def macs(self) -> float:
+        return float(sum(l.cin * l.cout * l.k * l.k * oh * ow
+                         for l, (oh, ow, _) in zip(self.layers, self.shapes)))
+
+    def forward(self, frame, state, scores, prev_mask, stream=None):
+        """frame, state [1, h, w, 3]; scores [1, h/4, w/4, c] (O_{t-1}); prev_mask uint8
+        [1, gh, gw] (A_{t-1}) or None. Returns P_t (self.prob, float32 [1, gh, gw])."""
+        bc.bc_policy_input(frame, state, scores, self.classes, prev_mask, self.grid, self.input,
+                           stream)
+        for i, l in enumerate(self.layers):
+            src = self.input if l.src < 0 else self.buffers[l.src]
+            res = None if l.res is None else self.buffers[l.res]
+            bc.bc_sparse_conv2d((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC,
+                                self.weights[i], self.biases[i], res, self.buffers[i],
+                                self.grids[i], None, None, stream)
+        bc.bc_policy_probabilities(self.buffers[-1], self.prob, stream)
+        return self.prob
+
+
 def layer_shapes(layers: list[Layer], h: int, w: int) -> list[tuple[int, int, int]]:
     """(out_h, out_w, out_c) of every layer for an h x w frame (the dense conv formula)."""
     shapes = []
@@ -179,20 +259,9 @@ class SparseResNet:
         self.h, self.w, self.block = h, w, block
         self.grid = (h // block, w // block)
         self.dtype, self.device = dtype, torch.device(device)
-        dcode = bc.BC_BF16 if dtype == torch.bfloat16 else bc.BC_F16
         params = params if params is not None else default_params(self.layers, seed0, bn_random)
         self.shapes = layer_shapes(self.layers, h, w)
-        self.weights, self.biases = [], []
-        for l, p in zip(self.layers, params):
-            if l.kind != "conv":
-                self.weights.append(None)
-                self.biases.append(None)
-                continue
-            wf, bf = bc.bc_fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
-            wr = bc.bc_repack_weights(wf.reshape(p["w"].shape), dcode)
-            wt = torch.from_numpy(wr.view(np.int16)).view(dtype).to(self.device)
-            self.weights.append(wt.contiguous())
-            self.biases.append(torch.from_numpy(bf).to(self.device))
+        self.weights, self.biases = device_weights(self.layers, params, dtype, self.device)
         self.buffers = [torch.empty((1, oh, ow, c), dtype=dtype, device=self.device)
                         for (oh, ow, c) in self.shapes]
         self.handles = [bc.Buffer(t, bc.BC_NHWC) for t in self.buffers]

@@ -29,7 +29,7 @@ def test_header_declares_the_boundary():
               "bc_sparse_maxpool2d", "bc_fold_bn", "bc_buffer_register", "bc_buffer_release",
               "bc_buffer_invalidate", "bc_buffer_mark_written", "bc_buffer_is_valid",
               "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
-              "bc_block_rewards", "bc_sparse_upsample_add"]:
+              "bc_block_rewards", "bc_sparse_upsample_add", "bc_policy_input", "bc_policy_probabilities"]:
         assert n in names
 
 
@@ -191,6 +191,25 @@ def test_policy_step_validation_codes(B):
     assert up(cap=127) == B.BC_ERR_CAPACITY
     assert up(out=FAKE_IN + 4096) == B.BC_ERR_ALIAS and up(skip=FAKE_OUT + 16) == B.BC_ERR_ALIAS
     assert up(idx=FAKE_OUT + 64) == B.BC_ERR_ALIAS
+    # policy network input and probabilities
+    fr, sc, po = B.bc_tensor(1, 3, 1024, 2048, 1, 1), B.bc_tensor(1, 64, 256, 512, 1, 1), B.bc_tensor(1, 32, 256, 512, 1, 1)
+    pin = lambda f=fr, c=sc, o=po, cls=19, gg=g, frame=FAKE_IN, out=FAKE_OUT, mask=FAKE_IDX: \
+        lib.bc_policy_input(frame, FAKE_W, f, FAKE_RES, c, cls, mask, gg, out, o, None)
+    assert pin(frame=None) == B.BC_ERR_NULL
+    assert pin(f=B.bc_tensor(1, 3, 1024, 2048, 1, 0)) == B.BC_ERR_LAYOUT
+    assert pin(c=B.bc_tensor(1, 64, 256, 512, 2, 1)) == B.BC_ERR_DTYPE
+    assert pin(f=B.bc_tensor(1, 4, 1024, 2048, 1, 1)) == B.BC_ERR_SHAPE
+    assert pin(c=B.bc_tensor(1, 64, 128, 512, 1, 1)) == B.BC_ERR_SHAPE
+    assert pin(o=B.bc_tensor(1, 16, 256, 512, 1, 1)) == B.BC_ERR_SHAPE
+    assert pin(cls=25) == B.BC_ERR_SHAPE and pin(cls=0) == B.BC_ERR_SHAPE
+    assert pin(c=B.bc_tensor(1, 20, 256, 512, 1, 1)) == B.BC_ERR_UNSUPPORTED
+    assert pin(gg=B.bc_grid(3, 16)) == B.BC_ERR_NOT_DIVISIBLE
+    assert pin(out=FAKE_W + 64) == B.BC_ERR_ALIAS
+    lg = B.bc_tensor(1, 64, 8, 16, 1, 1)
+    assert lib.bc_policy_probabilities(None, lg, FAKE_OUT, None) == B.BC_ERR_NULL
+    assert lib.bc_policy_probabilities(FAKE_IN, B.bc_tensor(1, 64, 8, 16, 0, 1), FAKE_OUT, None) == B.BC_ERR_DTYPE
+    assert lib.bc_policy_probabilities(FAKE_IN, B.bc_tensor(1, 64, 8, 16, 1, 0), FAKE_OUT, None) == B.BC_ERR_LAYOUT
+    assert lib.bc_policy_probabilities(FAKE_IN, lg, FAKE_IN + 64, None) == B.BC_ERR_ALIAS
     # rewards
     f = ctypes.c_float
     args = lambda **kw: [kw.get(k, v) for k, v in [("ig", FAKE_IN), ("mask", FAKE_W), ("prob", FAKE_RES), ("n", 1), ("g", g),
@@ -265,6 +284,7 @@ def test_runner_table_matches_oracle_table():
     from paper_2108_09376_amd import resnet
     pairs = [(onet.resnet_table(d), resnet.build_layers(d)) for d in (18, 50)]
     pairs += [(onet.swiftnet_table(d), resnet.build_swiftnet_layers(d)) for d in (18, 50)]
+    pairs += [(onet.policy_table(), resnet.build_policy_layers())]
     for a, b in pairs:
         assert len(a) == len(b)
         for x, y in zip(a, b):
