@@ -167,28 +167,28 @@ CASES = [
 ]
 
 
-def _conv_case(B, dtype, case, seed, integer=False, mask=None, prev=None):
+def _conv_case(B, dtype, case, seed, integer=False, mask=None, prev=None, n=1):
     cin, cout, h, w, gh, gw, k, s, relu, has_res, frac = case
     r = synth.rng(seed)
     p = k // 2
     ho, wo = oracle.out_size(h, k, s, p), oracle.out_size(w, k, s, p)
     if integer:
-        xv = synth.small_ints(r, (1, cin, h, w), -2, 2)
+        xv = synth.small_ints(r, (n, cin, h, w), -2, 2)
         wv = synth.small_ints(r, (cout, cin, k, k), -1, 1)
         bias = synth.small_ints(r, cout, -3, 3)
-        res = synth.small_ints(r, (1, cout, ho, wo), -4, 4) if has_res else None
+        res = synth.small_ints(r, (n, cout, ho, wo), -4, 4) if has_res else None
     else:
-        xv = synth.normal(r, (1, cin, h, w))
+        xv = synth.normal(r, (n, cin, h, w))
         wv = synth.he_normal(r, cout, cin, k, k)
         bias = synth.normal(r, cout, 0.1)
-        res = synth.normal(r, (1, cout, ho, wo)) if has_res else None
+        res = synth.normal(r, (n, cout, ho, wo)) if has_res else None
     x = synth.to_storage_bits(xv, dtype)
     wt = synth.to_storage_bits(wv, dtype)
     rb = None if res is None else synth.to_storage_bits(res, dtype)
     if prev is None:
-        prev = synth.nan_canaries(r, (1, cout, ho, wo), dtype)
+        prev = synth.nan_canaries(r, (n, cout, ho, wo), dtype)
     if mask is None:
-        mask = synth.frac_mask(seed + 1, gh, gw, frac)
+        mask = np.concatenate([synth.frac_mask(seed + 1 + i, gh, gw, frac) for i in range(n)])
     want = oracle.sparse_conv2d(x, wt, mask, prev, dtype, s, p, bias, rb, relu)
     idx, cnt, _ = _index(B, mask)
     out = to_dev(prev, dtype)
@@ -240,6 +240,17 @@ def test_conv_all_ones_equals_dense_call(B):
                        torch.from_numpy(bias).cuda(), to_dev(rb, "bf16"), out, (gh, gw), None, None)
     assert np.array_equal(from_dev(out), got)
     assert max_abs_rel(oracle.value(got, "bf16"), oracle.value(want, "bf16")) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("case", [CASES[0], CASES[2], CASES[3], CASES[7], CASES[12], CASES[11]],
+                         ids=["3x3_32px", "3x3_4px_P8", "1x1_two_chunks", "stem", "split_k", "ragged_tail"])
+def test_conv_mfma_batch(B, case):
+    """Three images in one call, each with its own execution grid: block ids span the
+    images (id = (img * Gh + gy) * Gw + gx)."""
+    got, want, mask, prev = _conv_case(B, "bf16", case, seed=95, n=3)
+    sel = block_select(mask, got.shape)
+    assert np.array_equal(got[~sel], prev[~sel])
+    assert max_abs_rel(oracle.value(got[sel], "bf16"), oracle.value(want[sel], "bf16")) <= TOL["bf16"]
 
 
 @pytest.mark.parametrize("case", [CASES[1], CASES[2], CASES[5], CASES[7]])
