@@ -30,6 +30,13 @@ excepted, see below), written from the paper's definitions:
   frame and the frame state averaged over 4x4 pixels, the class probabilities of
   O_{t-1}, A_{t-1} of the pixel's block, zeros); the network ends in a map with one
   pixel per block whose channel 0 is the block's logit, p_b = sigmoid(logit).
+* Section 4 (configuration): the policy is trained online with RMSprop (learning rate
+  1e-4, weight decay 1e-3), updating every 4 frames. The gradient is that of the
+  REINFORCE loss L = -sum_b R_b log pi(a_b) with pi(1) = p_b = sigmoid(z_b): dL/dz_b =
+  -R_b (a_b - p_b), back through the network's layers (readings: the batch-norm
+  statistics of the random initialisation are folded into the convolutions, which are
+  what is trained; RMSprop as PyTorch defines it, smoothing 0.99, eps 1e-8, weight
+  decay added to the gradient).
 * Section 3.5: rewards. R_IG = IG_b if a_b = 1, else -IG_b. C_t = fraction of executed
   blocks of the frame. M_t = (1 - mu) C_t + mu M_{t-1}, reading the printed C_{t-1} as
   the previous moving average M_{t-1} (the text calls M a moving average with
@@ -202,3 +209,60 @@ def policy_probabilities(logit_bits, dtype="bf16"):
     from . import value
     v = value(logit_bits, dtype)[:, 0]
     return 1.0 / (1.0 + np.exp(-v))
+
+
+def logit_grad(reward, mask, prob):
+    """dL/dz_b = -R_b (a_b - p_b) of the REINFORCE loss, p_b = sigmoid(z_b). [n, gh, gw]."""
+    a = (np.asarray(mask) != 0).astype(np.float64)
+    return -np.asarray(reward, np.float64) * (a - np.asarray(prob, np.float64))
+
+
+def policy_backward(table, weights, biases, x, dz):
+    """Gradients of L with respect to every layer's weights and bias, float64.
+
+    weights[l]: [cout, cin, k, k] (OIHW), biases[l]: [cout], x: S_t [n, 32, h, w] values,
+    dz: dL/dz [n, gh, gw] for channel 0 of the last layer. The forward pass is recomputed
+    in float64 (no storage rounding); the reverse pass visits the layers in reverse
+    order: through the ReLU (where the output is > 0), then the weight gradient (the
+    correlation of the layer's input with the output gradient), the bias gradient (its
+    sum) and the input gradient (the transposed convolution), added to every producer
+    that the layer reads (its source, and its residual source as is). torch's conv
+    primitives in float64 are the steps. Returns (dW list, db list)."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.grad import conv2d_input, conv2d_weight
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    xs = t(x)
+    ys = []
+    for l, w, b in zip(table, weights, biases):
+        src = xs if l["src"] < 0 else ys[l["src"]]
+        y = F.conv2d(src, t(w), t(b), stride=l["stride"], padding=l["pad"])
+        if l["res"] is not None:
+            y = y + ys[l["res"]]
+        ys.append(torch.relu(y) if l["relu"] else y)
+    g = [torch.zeros_like(y) for y in ys]
+    g[-1][:, 0] = t(dz)
+    dw, db = [None] * len(table), [None] * len(table)
+    for li in range(len(table) - 1, -1, -1):
+        l = table[li]
+        gp = g[li] * (ys[li] > 0) if l["relu"] else g[li]
+        src = xs if l["src"] < 0 else ys[l["src"]]
+        dw[li] = conv2d_weight(src, t(weights[li]).shape, gp, stride=l["stride"],
+                               padding=l["pad"]).numpy()
+        db[li] = gp.sum(dim=(0, 2, 3)).numpy()
+        if l["src"] >= 0:
+            g[l["src"]] += conv2d_input(src.shape, t(weights[li]), gp, stride=l["stride"],
+                                        padding=l["pad"])
+        if l["res"] is not None:
+            g[l["res"]] += gp
+    return dw, db
+
+
+def rmsprop_step(w, v, grad, lr=1e-4, alpha=0.99, eps=1e-8, weight_decay=1e-3):
+    """One RMSprop step as PyTorch defines it (no momentum, not centered):
+    g = grad + weight_decay * w; v = alpha v + (1 - alpha) g^2; w = w - lr g / (sqrt(v) + eps).
+    float64; returns (w, v)."""
+    w = np.asarray(w, np.float64)
+    g = np.asarray(grad, np.float64) + weight_decay * w
+    v = alpha * np.asarray(v, np.float64) + (1.0 - alpha) * g * g
+    return w - lr * g / (np.sqrt(v) + eps), v

@@ -1,7 +1,9 @@
 """Pins of the policy-network part of the oracle (Section 3.3, Eq. 2; the architecture
 reading is in oracle/policy.py): the assembly of S_t against per-pixel loops, library
 routines and exact constants, the sigmoid against scipy, the network table against the
-paper's cost figure, and the dense network against a torch-built reference."""
+paper's cost figure, and the dense network against a torch-built reference; for the
+online training, the reverse pass against central finite differences of the loss, the
+logit gradient against its closed form, and the RMSprop step against torch.optim."""
 import numpy as np
 import pytest
 import scipy.special
@@ -108,3 +110,79 @@ def test_policy_dense_network_equals_library_reference():
         g, wv = oracle.value(got[li], "bf16"), ref[li].numpy()
         assert (g != wv).mean() < 1e-3, li               # 1-ulp flips on rounding boundaries
         np.testing.assert_allclose(g, wv, rtol=2 ** -7, atol=1e-30)
+
+
+# ------------------------------------------------------------------ online training
+
+def _tiny_policy():
+    """The policy table's layer kinds at a few channels (fast finite differences):
+    stride-2 3x3, stride-1 3x3 with a residual, a 1x1/2 projection, a no-ReLU head."""
+    def conv(name, src, cin, cout, k, s, relu, res=None):
+        return dict(kind="conv", name=name, src=src, res=res, cin=cin, cout=cout, k=k,
+                    stride=s, pad=k // 2, relu=relu)
+    return [conv("stem", -1, 3, 4, 3, 2, True), conv("c1", 0, 4, 4, 3, 1, True, res=0),
+            conv("ds", 1, 4, 6, 1, 2, False), conv("c2", 1, 4, 6, 3, 2, True),
+            conv("c3", 3, 6, 6, 3, 1, True, res=2), conv("head", 4, 6, 2, 3, 2, False)]
+
+
+def _loss(table, ws, bs, x, dz):
+    """sum over blocks of dz * z (a linear functional with gradient dz at the logits)."""
+    ys = []
+    for l, w, b in zip(table, ws, bs):
+        src = x if l["src"] < 0 else ys[l["src"]]
+        y = F.conv2d(torch.from_numpy(src) if isinstance(src, np.ndarray) else src,
+                     torch.from_numpy(w), torch.from_numpy(b), stride=l["stride"], padding=l["pad"])
+        if l["res"] is not None:
+            y = y + ys[l["res"]]
+        ys.append(torch.relu(y) if l["relu"] else y)
+    return float((ys[-1][:, 0] * torch.from_numpy(dz)).sum())
+
+
+def test_policy_backward_finite_differences():
+    """Central differences of the loss against the reverse pass, per layer."""
+    table = _tiny_policy()
+    r = synth.rng(7)
+    ws = [r.normal(0, 0.5, (l["cout"], l["cin"], l["k"], l["k"])) for l in table]
+    bs = [r.normal(0, 0.1, l["cout"]) for l in table]
+    x = r.normal(0, 1, (1, 3, 16, 16))
+    dz = r.normal(0, 1, (1, 2, 2))
+    dw, db = P.policy_backward(table, ws, bs, x, dz)
+    h = 1e-6
+    for li in range(len(table)):
+        for _ in range(4):
+            idx = tuple(int(r.integers(0, s)) for s in ws[li].shape)
+            wp = [w.copy() for w in ws]
+            wm = [w.copy() for w in ws]
+            wp[li][idx] += h
+            wm[li][idx] -= h
+            fd = (_loss(table, wp, bs, x, dz) - _loss(table, wm, bs, x, dz)) / (2 * h)
+            assert abs(fd - dw[li][idx]) <= 1e-6 * max(1.0, abs(fd)), (li, idx)
+        c = int(r.integers(0, table[li]["cout"]))
+        bp = [b.copy() for b in bs]
+        bm = [b.copy() for b in bs]
+        bp[li][c] += h
+        bm[li][c] -= h
+        fd = (_loss(table, ws, bp, x, dz) - _loss(table, ws, bm, x, dz)) / (2 * h)
+        assert abs(fd - db[li][c]) <= 1e-6 * max(1.0, abs(fd)), (li, "bias")
+
+
+def test_logit_grad_closed_form():
+    """d/dz of -R log sigmoid(z) is -R (1 - p); of -R log(1 - sigmoid(z)) it is R p."""
+    r = np.array([[[2.0, -1.0]]])
+    p = np.array([[[0.25, 0.75]]])
+    g = P.logit_grad(r, np.array([[[1, 0]]], np.uint8), p)
+    np.testing.assert_allclose(g, [[[-2.0 * 0.75, -1.0 * 0.75]]])
+
+
+def test_rmsprop_matches_torch():
+    r = synth.rng(8)
+    w0 = r.normal(0, 1, 50)
+    grads = [r.normal(0, 1, 50) for _ in range(3)]
+    pt = torch.nn.Parameter(torch.from_numpy(w0.copy()))
+    opt = torch.optim.RMSprop([pt], lr=1e-4, alpha=0.99, eps=1e-8, weight_decay=1e-3)
+    w, v = w0.copy(), np.zeros(50)
+    for g in grads:
+        pt.grad = torch.from_numpy(g.copy())
+        opt.step()
+        w, v = P.rmsprop_step(w, v, g)
+    np.testing.assert_allclose(w, pt.detach().numpy(), rtol=1e-12, atol=1e-15)
