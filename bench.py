@@ -248,7 +248,10 @@ def policy_steps(torch, bc, dev):
                         once, the output blocks written once
       policy_forward    the policy network on a 2048x1024 frame (random init): S_t
                         assembly, eleven dense convolutions, the block probabilities;
-                        FLOPs = 2 x its MACs"""
+                        FLOPs = 2 x its MACs
+      policy_update     its online update at that forward pass: REINFORCE gradient of
+                        the logits, the reverse pass (ReLU masks, weight, bias and
+                        input gradients of every layer) and one RMSprop step"""
     import numpy as np
 
     import synth
@@ -294,6 +297,7 @@ def policy_steps(torch, bc, dev):
     pnet = resnet.PolicyNet(1024, 2048, device=dev)
     scores = torch.randn((1, 256, 512, 64), device=dev).to(torch.bfloat16)
     ops["policy_forward"] = (lambda: pnet.forward(frame, state, scores, mask), None)
+    ops["policy_update"] = (lambda: pnet.train_step(reward, mask, prob), None)
     out = {}
     for name, (fn, nbytes) in ops.items():
         fn()

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 4
+#define BC_ABI_VERSION 5
 
 typedef enum {
     BC_OK = 0,
@@ -340,6 +340,80 @@ bc_status bc_policy_input(const void *d_frame, const void *d_state, bc_tensor fr
  */
 bc_status bc_policy_probabilities(const void *d_logits, bc_tensor logits, float *d_prob,
                                   void *stream);
+
+/* ------------------------------------------------------------------------------
+ * Online training of the policy network (Section 4 configuration: RMSprop on the
+ * REINFORCE loss of Section 3.5, every 4 frames). Gradient maps are channels-last
+ * BF16/F16 like the activations; weight gradients and optimiser state are fp32.
+ * ------------------------------------------------------------------------------ */
+
+/*
+ * Gradient of the loss L = -sum_b R_b log pi(a_b) (pi(1) = p_b = sigmoid(z_b)) with
+ * respect to the head's logits: dL/dz_b = -R_b (a_b - p_b), written to channel 0 of
+ * d_grad [n][grid_h][grid_w][c] (desc: the head's output map); other channels 0.
+ *   d_reward, d_prob  float32 [n][grid_h][grid_w]; d_mask uint8 (nonzero = executed).
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS,
+ * BC_ERR_UNSUPPORTED (c % 8 != 0), BC_ERR_HIP.
+ */
+bc_status bc_policy_logit_grad(const float *d_reward, const uint8_t *d_mask, const float *d_prob,
+                               void *d_grad, bc_tensor grad, void *stream);
+
+/*
+ * d_out = (d_a + d_b) * [d_y > 0], elementwise in fp32, one round to the dtype; d_b
+ * and d_y may be NULL (then omitted). With d_y: the backward pass of a ReLU whose
+ * output is d_y; with d_b: two gradients of one tensor added. d_out may equal d_a or
+ * d_b. desc: NHWC BF16/F16 with c % 8 == 0 (all four tensors alike).
+ * Errors: BC_ERR_NULL, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS, BC_ERR_UNSUPPORTED,
+ * BC_ERR_HIP.
+ */
+bc_status bc_grad_combine(const void *d_a, const void *d_b, const void *d_y, bc_tensor desc,
+                          void *d_out, void *stream);
+
+/*
+ * Input gradient of a convolution (its transposed convolution) over every pixel:
+ *   d_grad_in = convT(d_grad_out, d_w) (+ d_accum if not NULL),
+ * for a layer with kernel k x k (k = 1 or 3), stride 1 or 2, pad k/2, weights d_w
+ * [cout][k][k][cin] in the map dtype. grad_in is the layer's input shape
+ * [n][h][w][cin] (cin % 64 == 0, h and w multiples of the stride, and of 8 when
+ * above 8), grad_out its output shape [n][h/s][w/s][cout] (cout % 64 == 0). Runs on
+ * the matrix-core convolution with flipped, transposed weights (and for stride 2 the
+ * output gradient spread onto even pixels) in a library-owned workspace, one per
+ * device, used in stream order (calls on different streams of one device race). The
+ * workspace grows (hipFree + hipMalloc) when a call needs more than it holds: a
+ * caller that captures calls into a graph makes one eager call at the largest size
+ * first, so no capture allocates and no captured pointer is freed later.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS
+ * (d_grad_in overlapping an input), BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ */
+bc_status bc_conv2d_input_grad(const bc_conv *geom, const void *d_grad_out, bc_tensor grad_out,
+                               const void *d_w, const void *d_accum, void *d_grad_in,
+                               bc_tensor grad_in, void *stream);
+
+/*
+ * Weight and bias gradients of a convolution, ADDED to d_dw and d_db:
+ *   d_dw[co][i][j][ci] += sum_p grad_out[p][co] * in[p*s - pad + (i, j)][ci],
+ *   d_db[co] += sum_p grad_out[p][co]    (d_db may be NULL).
+ * Geometry and shapes as bc_conv2d_input_grad (in: [n][h][w][cin], cin % 8 == 0).
+ * fp32 accumulation; partial sums are added with fp32 atomics, so the low bits of a
+ * result may differ between runs.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS,
+ * BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ */
+bc_status bc_conv2d_weight_grad(const bc_conv *geom, const void *d_in, bc_tensor in,
+                                const void *d_grad_out, bc_tensor grad_out, float *d_dw,
+                                float *d_db, void *stream);
+
+/*
+ * One RMSprop step over `count` fp32 parameters (PyTorch's definition, no momentum):
+ *   g = d_grad + weight_decay * w;  v = alpha v + (1 - alpha) g^2;
+ *   w = w - lr * g / (sqrt(v) + eps);  d_grad = 0;
+ * and, if d_w16 is not NULL, its 16-bit copy (dtype BC_BF16 or BC_F16, round to
+ * nearest even) rewritten, e.g. the weights the convolutions read.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_ALIAS, BC_ERR_HIP.
+ */
+bc_status bc_rmsprop_step(float *d_w, float *d_v, float *d_grad, int64_t count, float lr,
+                          float alpha, float eps, float weight_decay, void *d_w16, int32_t dtype,
+                          void *stream);
 
 /*
  * Block rewards and the policy loss (Section 3.5), per image n of the batch:

@@ -217,12 +217,14 @@ def logit_grad(reward, mask, prob):
     return -np.asarray(reward, np.float64) * (a - np.asarray(prob, np.float64))
 
 
-def policy_backward(table, weights, biases, x, dz):
+def policy_backward(table, weights, biases, x, dz, stored=None):
     """Gradients of L with respect to every layer's weights and bias, float64.
 
     weights[l]: [cout, cin, k, k] (OIHW), biases[l]: [cout], x: S_t [n, 32, h, w] values,
-    dz: dL/dz [n, gh, gw] for channel 0 of the last layer. The forward pass is recomputed
-    in float64 (no storage rounding); the reverse pass visits the layers in reverse
+    dz: dL/dz [n, gh, gw] for channel 0 of the last layer. The reverse pass uses the
+    forward pass's activations: `stored` (one array of values per layer, e.g. the
+    storage-rounded maps a forward pass kept, as the device keeps them), or, if None,
+    the forward pass recomputed in float64 without rounding. It visits the layers in reverse
     order: through the ReLU (where the output is > 0), then the weight gradient (the
     correlation of the layer's input with the output gradient), the bias gradient (its
     sum) and the input gradient (the transposed convolution), added to every producer
@@ -234,12 +236,15 @@ def policy_backward(table, weights, biases, x, dz):
     t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
     xs = t(x)
     ys = []
-    for l, w, b in zip(table, weights, biases):
-        src = xs if l["src"] < 0 else ys[l["src"]]
-        y = F.conv2d(src, t(w), t(b), stride=l["stride"], padding=l["pad"])
-        if l["res"] is not None:
-            y = y + ys[l["res"]]
-        ys.append(torch.relu(y) if l["relu"] else y)
+    if stored is not None:
+        ys = [t(a) for a in stored]
+    else:
+        for l, w, b in zip(table, weights, biases):
+            src = xs if l["src"] < 0 else ys[l["src"]]
+            y = F.conv2d(src, t(w), t(b), stride=l["stride"], padding=l["pad"])
+            if l["res"] is not None:
+                y = y + ys[l["res"]]
+            ys.append(torch.relu(y) if l["relu"] else y)
     g = [torch.zeros_like(y) for y in ys]
     g[-1][:, 0] = t(dz)
     dw, db = [None] * len(table), [None] * len(table)

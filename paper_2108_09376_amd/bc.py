@@ -76,6 +76,11 @@ _sigs = {
     "bc_seg_information_gain": ([_vp, _vp, bc_tensor, _i32, bc_grid, _vp, _vp], _i32),
     "bc_policy_input": ([_vp, _vp, bc_tensor, _vp, bc_tensor, _i32, _vp, bc_grid, _vp, bc_tensor, _vp], _i32),
     "bc_policy_probabilities": ([_vp, bc_tensor, _vp, _vp], _i32),
+    "bc_policy_logit_grad": ([_vp, _vp, _vp, _vp, bc_tensor, _vp], _i32),
+    "bc_grad_combine": ([_vp, _vp, _vp, bc_tensor, _vp, _vp], _i32),
+    "bc_conv2d_input_grad": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, bc_tensor, _vp], _i32),
+    "bc_conv2d_weight_grad": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, _vp, _vp, _vp], _i32),
+    "bc_rmsprop_step": ([_vp, _vp, _vp, ctypes.c_int64, _f32, _f32, _f32, _f32, _vp, _i32, _vp], _i32),
     "bc_block_rewards": ([_vp, _vp, _vp, _i32, bc_grid, _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
@@ -87,7 +92,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 4
+ABI_VERSION = 5
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -268,6 +273,44 @@ def bc_policy_probabilities(logits, prob, stream=None):
     """prob float32 [n, gh, gw] = sigmoid(logits[..., 0]), logits [n, gh, gw, c] NHWC."""
     st = _lib.bc_policy_probabilities(_ptr(logits), desc(logits, BC_NHWC), _ptr(prob), _stream(stream))
     _check(st, "bc_policy_probabilities")
+
+
+def bc_policy_logit_grad(reward, mask, prob, grad, stream=None):
+    """grad [n, gh, gw, c] NHWC: channel 0 = -R (a - p), the rest 0."""
+    st = _lib.bc_policy_logit_grad(_ptr(reward), _ptr(mask), _ptr(prob), _ptr(grad),
+                                   desc(grad, BC_NHWC), _stream(stream))
+    _check(st, "bc_policy_logit_grad")
+
+
+def bc_grad_combine(a, b, y, out, stream=None):
+    """out = (a + b) * [y > 0] (b, y may be None); NHWC 16-bit, all alike."""
+    st = _lib.bc_grad_combine(_ptr(a), _ptr(b), _ptr(y), desc(a, BC_NHWC), _ptr(out), _stream(stream))
+    _check(st, "bc_grad_combine")
+
+
+def bc_conv2d_input_grad(geom, grad_out, w, accum, grad_in, stream=None):
+    """grad_in = transposed conv of grad_out with w (+ accum), NHWC."""
+    c = _conv(geom)
+    st = _lib.bc_conv2d_input_grad(ctypes.byref(c), _ptr(grad_out), desc(grad_out, BC_NHWC), _ptr(w),
+                                   _ptr(accum), _ptr(grad_in), desc(grad_in, BC_NHWC), _stream(stream))
+    _check(st, "bc_conv2d_input_grad")
+
+
+def bc_conv2d_weight_grad(geom, x, grad_out, dw, db=None, stream=None):
+    """dw float32 [cout, k, k, cin] += weight gradient; db float32 [cout] += bias gradient."""
+    c = _conv(geom)
+    st = _lib.bc_conv2d_weight_grad(ctypes.byref(c), _ptr(x), desc(x, BC_NHWC), _ptr(grad_out),
+                                    desc(grad_out, BC_NHWC), _ptr(dw), _ptr(db), _stream(stream))
+    _check(st, "bc_conv2d_weight_grad")
+
+
+def bc_rmsprop_step(w, v, grad, lr, alpha, eps, weight_decay, w16=None, stream=None):
+    """One RMSprop step on float32 tensors w, v, grad (grad reset to 0), and the 16-bit
+    copy w16 (same element count) if given."""
+    dt = _dtype_code(w16) if w16 is not None else BC_BF16
+    st = _lib.bc_rmsprop_step(_ptr(w), _ptr(v), _ptr(grad), ctypes.c_int64(int(w.numel())), float(lr),
+                              float(alpha), float(eps), float(weight_decay), _ptr(w16), dt, _stream(stream))
+    _check(st, "bc_rmsprop_step")
 
 
 def bc_block_rewards(ig, mask, prob, grid, tau, gamma, mu, mavg, reward, cost=None, loss=None,

@@ -2,6 +2,7 @@
 // error text, the persistent-buffer registry and kernel dispatch. Every check runs
 // before anything is enqueued; kernels are launched on the caller's stream.
 #include <math.h>
+#include <cmath>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -686,6 +687,148 @@ bc_status bc_policy_probabilities(const void *d_logits, bc_tensor logits, float 
     hipError_t e = bc::launch_policy_probabilities(d_logits, (int)blocks, logits.c,
                                                    logits.dtype == BC_BF16, d_prob, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "policy probabilities launch");
+    return ok();
+}
+
+// ---------------------------------------------------------------- policy training
+
+static bc_status check_grad_map(const bc_tensor &t, const char *name)
+{
+    bc_status st = check_tensor(t, name);
+    if (st) return st;
+    if (t.layout != BC_NHWC) return fail(BC_ERR_LAYOUT, "%s must be channels last", name);
+    if (t.dtype == BC_F32) return fail(BC_ERR_DTYPE, "%s must be bf16 or f16", name);
+    if (t.c % 8) return fail(BC_ERR_UNSUPPORTED, "%s: channels must be a multiple of 8", name);
+    return BC_OK;
+}
+
+bc_status bc_policy_logit_grad(const float *d_reward, const uint8_t *d_mask, const float *d_prob,
+                               void *d_grad, bc_tensor grad, void *stream)
+{
+    if (!d_reward || !d_mask || !d_prob || !d_grad)
+        return fail(BC_ERR_NULL, "d_reward, d_mask, d_prob and d_grad are required");
+    bc_status st;
+    if ((st = check_grad_map(grad, "grad"))) return st;
+    const double blocks = (double)grad.n * grad.h * grad.w;
+    if (blocks > (double)(1 << 20)) return fail(BC_ERR_SHAPE, "more than 2^20 blocks");
+    const size_t gb = tensor_bytes(grad), nb = (size_t)blocks;
+    if (overlap(d_grad, gb, d_reward, nb * 4) || overlap(d_grad, gb, d_prob, nb * 4) ||
+        overlap(d_grad, gb, d_mask, nb))
+        return fail(BC_ERR_ALIAS, "d_grad overlaps an input");
+    hipError_t e = bc::launch_logit_grad(d_reward, d_mask, d_prob, d_grad, (int)blocks, grad.c,
+                                         grad.dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "logit gradient launch");
+    return ok();
+}
+
+bc_status bc_grad_combine(const void *d_a, const void *d_b, const void *d_y, bc_tensor desc,
+                          void *d_out, void *stream)
+{
+    if (!d_a || !d_out) return fail(BC_ERR_NULL, "d_a and d_out are required");
+    bc_status st;
+    if ((st = check_grad_map(desc, "desc"))) return st;
+    const size_t bytes = tensor_bytes(desc);
+    // out may equal a or b (elementwise, each element read before it is written), not
+    // partially overlap them
+    auto bad = [&](const void *p) { return p && p != d_out && overlap(d_out, bytes, p, bytes); };
+    if (bad(d_a) || bad(d_b) || bad(d_y)) return fail(BC_ERR_ALIAS, "d_out partially overlaps an input");
+    hipError_t e = bc::launch_grad_combine(d_a, d_b, d_y, d_out, (long long)bytes / 2,
+                                           desc.dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "gradient combine launch");
+    return ok();
+}
+
+// The forward layer of a backward call: input `in`, output gradient `gout` (shaped like
+// the layer's output), geometry k x k, stride, pad = k / 2.
+static bc_status train_geom(const bc_conv *geom, const bc_tensor &in, const bc_tensor &gout,
+                            bc::LayerGeom &L)
+{
+    if (!geom) return fail(BC_ERR_NULL, "geometry is required");
+    bc_status st;
+    if ((st = check_grad_map(in, "in"))) return st;
+    if ((st = check_grad_map(gout, "grad_out"))) return st;
+    if (in.dtype != gout.dtype) return fail(BC_ERR_DTYPE, "in and grad_out dtypes differ");
+    if (geom->kh != geom->kw || (geom->kh != 1 && geom->kh != 3))
+        return fail(BC_ERR_UNSUPPORTED, "kernel must be 1x1 or 3x3");
+    if (geom->stride != 1 && geom->stride != 2) return fail(BC_ERR_UNSUPPORTED, "stride must be 1 or 2");
+    if (geom->pad != geom->kh / 2) return fail(BC_ERR_UNSUPPORTED, "pad must be k / 2");
+    if (gout.n != in.n || gout.h * geom->stride != in.h || gout.w * geom->stride != in.w)
+        return fail(BC_ERR_SHAPE, "grad_out must be the layer's output: [n][h/s][w/s][cout] with h, w "
+                                  "multiples of the stride");
+    if (gout.c % 64) return fail(BC_ERR_UNSUPPORTED, "output channels must be a multiple of 64");
+    L.n = in.n; L.cin = in.c; L.hin = in.h; L.win = in.w;
+    L.cout = gout.c; L.hout = gout.h; L.wout = gout.w;
+    L.kh = geom->kh; L.kw = geom->kw; L.stride = geom->stride; L.pad = geom->pad;
+    L.gh = L.gw = 1; L.bh = gout.h; L.bw = gout.w; L.total_blocks = in.n;
+    L.idx = nullptr; L.count = nullptr;
+    if (tensor_bytes(in) >= 2147483392u || tensor_bytes(gout) >= 2147483392u)
+        return fail(BC_ERR_UNSUPPORTED, "tensors must be below 2 GiB");
+    return BC_OK;
+}
+
+bc_status bc_conv2d_input_grad(const bc_conv *geom, const void *d_grad_out, bc_tensor grad_out,
+                               const void *d_w, const void *d_accum, void *d_grad_in,
+                               bc_tensor grad_in, void *stream)
+{
+    if (!d_grad_out || !d_w || !d_grad_in)
+        return fail(BC_ERR_NULL, "d_grad_out, d_w and d_grad_in are required");
+    bc::LayerGeom L;
+    bc_status st = train_geom(geom, grad_in, grad_out, L);
+    if (st) return st;
+    if (grad_in.c % 64) return fail(BC_ERR_UNSUPPORTED, "input channels must be a multiple of 64");
+    if (grad_in.h % 8 && grad_in.h > 8) return fail(BC_ERR_UNSUPPORTED, "input height must be <= 8 or a multiple of 8");
+    if (grad_in.w % 8 && grad_in.w > 8) return fail(BC_ERR_UNSUPPORTED, "input width must be <= 8 or a multiple of 8");
+    const size_t ib = tensor_bytes(grad_in), ob = tensor_bytes(grad_out);
+    const size_t wb = (size_t)grad_out.c * geom->kh * geom->kw * grad_in.c * 2;
+    if (overlap(d_grad_in, ib, d_grad_out, ob) || overlap(d_grad_in, ib, d_w, wb) ||
+        overlap(d_grad_in, ib, d_accum, ib))
+        return fail(BC_ERR_ALIAS, "d_grad_in overlaps an input");
+    const char *why = "";
+    hipError_t e = bc::launch_conv_input_grad(
+        (const uint16_t *)d_grad_out, (const uint16_t *)d_w, (const uint16_t *)d_accum,
+        (uint16_t *)d_grad_in, L, grad_in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16,
+        (hipStream_t)stream, &why);
+    if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
+    if (e != hipSuccess) return hip_fail(e, "input gradient launch");
+    return ok();
+}
+
+bc_status bc_conv2d_weight_grad(const bc_conv *geom, const void *d_in, bc_tensor in,
+                                const void *d_grad_out, bc_tensor grad_out, float *d_dw,
+                                float *d_db, void *stream)
+{
+    if (!d_in || !d_grad_out || !d_dw) return fail(BC_ERR_NULL, "d_in, d_grad_out and d_dw are required");
+    bc::LayerGeom L;
+    bc_status st = train_geom(geom, in, grad_out, L);
+    if (st) return st;
+    const double wgs = (double)(grad_out.c / 64) * ((in.c + 63) / 64) * geom->kh * geom->kw *
+                       std::ceil((double)in.n * grad_out.h * grad_out.w / 1024.0);
+    if (wgs >= 4194304.0) return fail(BC_ERR_UNSUPPORTED, "too many pixels for one call");
+    const size_t dwb = (size_t)grad_out.c * geom->kh * geom->kw * in.c * 4;
+    if (overlap(d_dw, dwb, d_in, tensor_bytes(in)) || overlap(d_dw, dwb, d_grad_out, tensor_bytes(grad_out)) ||
+        overlap(d_db, (size_t)grad_out.c * 4, d_dw, dwb))
+        return fail(BC_ERR_ALIAS, "gradient outputs overlap each other or an input");
+    hipError_t e = bc::launch_conv_weight_grad((const uint16_t *)d_in, (const uint16_t *)d_grad_out,
+                                               d_dw, d_db, L, in.dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "weight gradient launch");
+    return ok();
+}
+
+bc_status bc_rmsprop_step(float *d_w, float *d_v, float *d_grad, int64_t count, float lr,
+                          float alpha, float eps, float weight_decay, void *d_w16, int32_t dtype,
+                          void *stream)
+{
+    if (!d_w || !d_v || !d_grad) return fail(BC_ERR_NULL, "d_w, d_v and d_grad are required");
+    if (count <= 0 || count > ((int64_t)1 << 31)) return fail(BC_ERR_SHAPE, "count outside 1..2^31");
+    if (d_w16 && dtype != BC_BF16 && dtype != BC_F16) return fail(BC_ERR_DTYPE, "the copy must be bf16 or f16");
+    const size_t b = (size_t)count * 4;
+    if (overlap(d_w, b, d_v, b) || overlap(d_w, b, d_grad, b) || overlap(d_v, b, d_grad, b) ||
+        overlap(d_w16, (size_t)count * 2, d_w, b) || overlap(d_w16, (size_t)count * 2, d_v, b) ||
+        overlap(d_w16, (size_t)count * 2, d_grad, b))
+        return fail(BC_ERR_ALIAS, "the optimiser's buffers overlap");
+    hipError_t e = bc::launch_rmsprop(d_w, d_v, d_grad, (long long)count, lr, alpha, eps, weight_decay,
+                                      d_w16, dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "rmsprop launch");
     return ok();
 }
 

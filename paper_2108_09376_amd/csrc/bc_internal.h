@@ -78,4 +78,18 @@ hipError_t launch_policy_input(const void *frame, const void *state, const void 
 hipError_t launch_policy_probabilities(const void *logits, int blocks, int c, bool bf16,
                                        float *prob, hipStream_t s);
 
+// Policy training: logit gradient, gradient combine, conv input / weight gradients,
+// RMSprop (k_train.hip).
+hipError_t launch_logit_grad(const float *reward, const uint8_t *mask, const float *prob,
+                             void *grad, int blocks, int c, bool bf16, hipStream_t s);
+hipError_t launch_grad_combine(const void *a, const void *b, const void *y, void *out,
+                               long long elems, bool bf16, hipStream_t s);
+hipError_t launch_conv_input_grad(const uint16_t *grad_out, const uint16_t *w, const uint16_t *accum,
+                                  uint16_t *grad_in, const LayerGeom &fwd, Half16 fmt,
+                                  hipStream_t s, const char **why);
+hipError_t launch_conv_weight_grad(const uint16_t *x, const uint16_t *g, float *dw, float *db,
+                                   const LayerGeom &fwd, bool bf16, hipStream_t s);
+hipError_t launch_rmsprop(float *w, float *v, float *grad, long long count, float lr, float alpha,
+                          float eps, float wd, void *w16, bool bf16, hipStream_t s);
+
 }  // namespace bc

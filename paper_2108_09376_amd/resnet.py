@@ -208,6 +208,68 @@ class PolicyNet:
         bc.bc_policy_probabilities(self.buffers[-1], self.prob, stream)
         return self.prob
 
+    # ------------------------------------------------------------------ online update
+    def _init_training(self):
+        """fp32 master weights ([cout][k][k][cin], the layout the convolutions read),
+        RMSprop state and gradient accumulators, and two gradient maps per layer."""
+        dev, dt = self.device, self.dtype
+        self.master, self.v_w, self.dw, self.v_b, self.db = [], [], [], [], []
+        for wt in self.weights:
+            m = wt.float().contiguous()
+            self.master.append(m)
+            self.v_w.append(torch.zeros_like(m))
+            self.dw.append(torch.zeros_like(m))
+        for b in self.biases:
+            self.v_b.append(torch.zeros_like(b))
+            self.db.append(torch.zeros_like(b))
+        self.gbufs = [[torch.empty((1, oh, ow, c), dtype=dt, device=dev) for _ in range(2)]
+                      for (oh, ow, c) in self.shapes]
+
+    def backward(self, reward, mask, prob, stream=None):
+        """Adds the gradients of L = -sum_b R_b log pi(a_b) at the last forward pass to
+        self.dw / self.db. reward, prob float32 [1, gh, gw]; mask uint8 (the executed
+        grid a_b)."""
+        if not hasattr(self, "master"):
+            self._init_training()
+        last = len(self.layers) - 1
+        cur = {last: self.gbufs[last][0]}
+        bc.bc_policy_logit_grad(reward, mask, prob, cur[last], stream)
+        for li in range(last, -1, -1):
+            l = self.layers[li]
+            gp = cur.pop(li)                          # complete: every consumer came later
+            if l.relu:
+                bc.bc_grad_combine(gp, None, self.buffers[li], gp, stream)
+            geom = (l.k, l.k, l.stride, l.pad, 0)
+            src = self.input if l.src < 0 else self.buffers[l.src]
+            bc.bc_conv2d_weight_grad(geom, src, gp, self.dw[li], self.db[li], stream)
+            if l.src >= 0:
+                acc = cur.get(l.src)
+                out = self.gbufs[l.src][1] if acc is self.gbufs[l.src][0] else self.gbufs[l.src][0]
+                bc.bc_conv2d_input_grad(geom, gp, self.weights[li], acc, out, stream)
+                cur[l.src] = out
+            if l.res is not None:
+                acc = cur.get(l.res)
+                if acc is None:
+                    cur[l.res] = self.gbufs[l.res][0]
+                    bc.bc_grad_combine(gp, None, None, cur[l.res], stream)
+                else:
+                    bc.bc_grad_combine(acc, gp, None, acc, stream)
+
+    def update(self, lr=1e-4, alpha=0.99, eps=1e-8, weight_decay=1e-3, stream=None):
+        """One RMSprop step on every weight and bias with the accumulated gradients (which
+        it resets); the 16-bit weights the convolutions read are rewritten."""
+        for i in range(len(self.layers)):
+            bc.bc_rmsprop_step(self.master[i], self.v_w[i], self.dw[i], lr, alpha, eps, weight_decay,
+                               self.weights[i], stream)
+            bc.bc_rmsprop_step(self.biases[i], self.v_b[i], self.db[i], lr, alpha, eps, weight_decay,
+                               None, stream)
+
+    def train_step(self, reward, mask, prob, stream=None, **rmsprop):
+        """The online update of Section 4: backward pass at the last forward pass, then one
+        RMSprop step."""
+        self.backward(reward, mask, prob, stream)
+        self.update(stream=stream, **rmsprop)
+
 
 def layer_shapes(layers: list[Layer], h: int, w: int) -> list[tuple[int, int, int]]:
     """(out_h, out_w, out_c) of every layer for an h x w frame (the dense conv formula)."""

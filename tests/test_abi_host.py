@@ -29,7 +29,9 @@ def test_header_declares_the_boundary():
               "bc_sparse_maxpool2d", "bc_fold_bn", "bc_buffer_register", "bc_buffer_release",
               "bc_buffer_invalidate", "bc_buffer_mark_written", "bc_buffer_is_valid",
               "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
-              "bc_block_rewards", "bc_sparse_upsample_add", "bc_policy_input", "bc_policy_probabilities"]:
+              "bc_block_rewards", "bc_sparse_upsample_add", "bc_policy_input", "bc_policy_probabilities",
+              "bc_policy_logit_grad", "bc_grad_combine", "bc_conv2d_input_grad", "bc_conv2d_weight_grad",
+              "bc_rmsprop_step"]:
         assert n in names
 
 

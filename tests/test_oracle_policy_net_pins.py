@@ -166,6 +166,30 @@ def test_policy_backward_finite_differences():
         assert abs(fd - db[li][c]) <= 1e-6 * max(1.0, abs(fd)), (li, "bias")
 
 
+def test_policy_backward_with_stored_activations():
+    """Handing the reverse pass the exact forward activations changes nothing; handing it
+    storage-rounded ones changes the result only through those activations."""
+    table = _tiny_policy()
+    r = synth.rng(9)
+    ws = [r.normal(0, 0.5, (l["cout"], l["cin"], l["k"], l["k"])) for l in table]
+    bs = [r.normal(0, 0.1, l["cout"]) for l in table]
+    x = r.normal(0, 1, (1, 3, 16, 16))
+    dz = r.normal(0, 1, (1, 2, 2))
+    ys = []
+    for l, w, b in zip(table, ws, bs):
+        src = torch.from_numpy(x) if l["src"] < 0 else ys[l["src"]]
+        y = F.conv2d(src, torch.from_numpy(w), torch.from_numpy(b), stride=l["stride"], padding=l["pad"])
+        if l["res"] is not None:
+            y = y + ys[l["res"]]
+        ys.append(torch.relu(y) if l["relu"] else y)
+    a = P.policy_backward(table, ws, bs, x, dz)
+    b = P.policy_backward(table, ws, bs, x, dz, stored=[y.numpy() for y in ys])
+    for u, v in zip(a[0] + a[1], b[0] + b[1]):
+        assert np.array_equal(u, v)
+    c = P.policy_backward(table, ws, bs, x, dz, stored=[oracle.value(oracle.store(y.numpy(), "bf16"), "bf16") for y in ys])
+    assert not all(np.array_equal(u, v) for u, v in zip(a[0], c[0]))
+
+
 def test_logit_grad_closed_form():
     """d/dz of -R log sigmoid(z) is -R (1 - p); of -R log(1 - sigmoid(z)) it is R p."""
     r = np.array([[[2.0, -1.0]]])
