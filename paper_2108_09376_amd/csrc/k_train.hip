@@ -13,14 +13,17 @@
 //    stride-1 convolution with padding k/2 (these two kernels are here);
 //  * weight gradient: dW[co][i][j][ci] += sum_p G[p][co] X[p*s - pad + (i, j)][ci], an
 //    implicit GEMM whose reduction runs over pixels. A workgroup owns a 64 x 64
-//    (co, ci) tile of one tap and a range of pixels; per 32-pixel chunk it loads G and
-//    the tap-shifted X rows with 16-byte requests (eight channels of one pixel per lane)
-//    and stores them transposed in LDS ([channel][pixel], one 64-byte row per
-//    channel), so that matrix-core fragments (eight consecutive pixels of one channel
-//    per lane) are contiguous 16-byte LDS reads; two chunks in flight (registers and a
-//    double buffer); the tile is added to dW with fp32 atomics at the end (the order
-//    of those additions varies between runs);
-//  * bias gradient: db[co] += sum_p G[p][co];
+//    (co, ci) tile of one tap and a range of 1024 pixels; per 128-pixel chunk it loads
+//    G and the tap-shifted X rows with 16-byte requests (eight channels of one pixel),
+//    transposes them in registers and stores them in LDS as [channel][pixel], so that
+//    matrix-core fragments (eight consecutive pixels of one channel per lane) are
+//    contiguous 16-byte LDS reads; the next two chunks' loads are in flight during the
+//    current chunk's 16 MFMAs per wave (registers plus an LDS double buffer); the tile
+//    is added to dW with fp32 atomics at the end (the order of those additions varies
+//    between runs);
+//  * bias gradient: db[co] += sum_p G[p][co], summed from the same G registers by the
+//    workgroups of tap 0 (and the first ci tile), reduced across lanes, one atomic per
+//    channel and workgroup;
 //  * RMSprop (PyTorch's definition, no momentum): g' = g + wd w; v = alpha v +
 //    (1 - alpha) g'^2; w -= lr g' / (sqrt(v) + eps); the gradient is reset to 0 and the
 //    16-bit copy of w rewritten (round to nearest even).
@@ -161,9 +164,9 @@ __global__ __launch_bounds__(kThreads) void k_zero_insert16(const uint4 *__restr
 
 // ---------------------------------------------------------------- weight gradient
 
-constexpr int kPx = 32;                       // pixels per chunk (one MFMA k step)
+constexpr int kPx = 128;                      // pixels per chunk (four MFMA k steps)
 constexpr int kRow = kPx * 2 + 16;            // LDS bytes per channel row (+16 pad)
-constexpr int kWgPx = 1024;                   // pixels per workgroup (32 chunks)
+constexpr int kWgPx = 1024;                   // pixels per workgroup (8 chunks)
 
 struct WgradGeom {
     int n, hin, win, cin, hout, wout, cout, k, stride, pad;
@@ -172,13 +175,20 @@ struct WgradGeom {
     int x_bytes, g_bytes;
 };
 
+// LDS per chunk: G and X transposed, [channel][pixel], 64 rows of kRow bytes each. A
+// thread holds eight channels (vector cv) of four consecutive pixels (quad pq) of each
+// tensor and writes each channel's four pixels as one 8-byte word. With pq the fast
+// index over a wave's lanes and a row pitch of 68 dwords, those writes and the MFMA
+// fragment reads (16 rows at one column) are both free of bank conflicts.
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void k_wgrad16(const uint16_t *__restrict__ x,
                                                       const uint16_t *__restrict__ g,
-                                                      float *__restrict__ dw, WgradGeom G)
+                                                      float *__restrict__ dw, float *__restrict__ db,
+                                                      WgradGeom G)
 {
     __shared__ __align__(16) uint8_t lds[2][2][64 * kRow];   // [buffer][G, X][channel][pixel]
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     // blockIdx.x = ((co tile * ci tiles + ci tile) * taps + tap) * splits + split
     const int ci_tiles = (G.cin + 63) / 64, taps = G.k * G.k;
@@ -192,38 +202,73 @@ __global__ __launch_bounds__(kThreads) void k_wgrad16(const uint16_t *__restrict
     const int ti = tap / G.k, tj = tap - ti * G.k;
     const int p_lo = split * kWgPx, p_hi = min(G.npix, p_lo + kWgPx);
     const int nch = (p_hi - p_lo + kPx - 1) / kPx;
+    // the bias gradient comes from the first ci tile's tap-0 workgroups
+    const bool bias = db != nullptr && cit == 0 && tap == 0;
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
         (void *)x, (short)0, G.x_bytes, kBufferFlags);
     const __amdgpu_buffer_rsrc_t rg = __builtin_amdgcn_make_buffer_rsrc(
         (void *)g, (short)0, G.g_bytes, kBufferFlags);
-    // this thread loads eight channels (vector cv) of pixel px of each chunk
-    const int px = tid >> 3, cv = tid & 7;
-    auto load = [&](int c, uint4 &vg, uint4 &vx) {
-        const int p = p_lo + c * kPx + px;
-        int og = kOutOfRange, ox = kOutOfRange;
-        if (c < nch && p < p_hi) {
-            const int img = p / (G.hout * G.wout);
-            const int rem = p - img * G.hout * G.wout;
-            const int oy = rem / G.wout, oxx = rem - oy * G.wout;
-            og = (p * G.cout + co0 + cv * 8) * 2;
-            const int iy = oy * G.stride - G.pad + ti, ix = oxx * G.stride - G.pad + tj;
-            if (iy >= 0 && iy < G.hin && ix >= 0 && ix < G.win && ci0 + cv * 8 < G.cin)
-                ox = (((img * G.hin + iy) * G.win + ix) * G.cin + ci0 + cv * 8) * 2;
+    const int pq = tid & 31, cv = tid >> 5;
+    const int hw = G.hout * G.wout;
+    const bool ci_ok = ci0 + cv * 8 < G.cin;
+    auto load = [&](int c, i32x4 (&vg)[4], i32x4 (&vx)[4]) {
+        const int p0 = p_lo + c * kPx + 4 * pq;
+        int img = 0, oy = 0, ox = 0;
+        if (p0 < p_hi) {
+            img = p0 / hw;
+            const int rem = p0 - img * hw;
+            oy = rem / G.wout;
+            ox = rem - oy * G.wout;
         }
-        asm volatile("" : "+v"(og), "+v"(ox));
-        const i32x4 a = __builtin_amdgcn_raw_buffer_load_b128(rg, og, 0, 0);
-        const i32x4 b = __builtin_amdgcn_raw_buffer_load_b128(rx, ox, 0, 0);
-        vg = make_uint4((uint32_t)a[0], (uint32_t)a[1], (uint32_t)a[2], (uint32_t)a[3]);
-        vx = make_uint4((uint32_t)b[0], (uint32_t)b[1], (uint32_t)b[2], (uint32_t)b[3]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int p = p0 + j;
+            int og = kOutOfRange, oi = kOutOfRange;
+            if (p < p_hi) {
+                og = (p * G.cout + co0 + cv * 8) * 2;
+                const int iy = oy * G.stride - G.pad + ti, ix = ox * G.stride - G.pad + tj;
+                if (iy >= 0 && iy < G.hin && ix >= 0 && ix < G.win && ci_ok)
+                    oi = (((img * G.hin + iy) * G.win + ix) * G.cin + ci0 + cv * 8) * 2;
+            }
+            asm volatile("" : "+v"(og), "+v"(oi));
+            vg[j] = __builtin_amdgcn_raw_buffer_load_b128(rg, og, 0, 0);
+            vx[j] = __builtin_amdgcn_raw_buffer_load_b128(rx, oi, 0, 0);
+            if (++ox == G.wout) {
+                ox = 0;
+                if (++oy == G.hout) {
+                    oy = 0;
+                    ++img;
+                }
+            }
+        }
     };
-    // transposed store: channel cv*8 + e, pixel px
-    auto store = [&](int buf, const uint4 &vg, const uint4 &vx) {
-        const uint32_t gg[4] = {vg.x, vg.y, vg.z, vg.w}, xx[4] = {vx.x, vx.y, vx.z, vx.w};
+    float bsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    // channel e of the four pixels: halves e&1 of dword e>>1, pixels 0..3 -> one 8-byte word
+    auto pack = [](const i32x4 (&v)[4], int e) {
+        const int w = e >> 1;
+        uint2 o;
+        if (e & 1) {
+            o.x = ((uint32_t)v[0][w] >> 16) | ((uint32_t)v[1][w] & 0xFFFF0000u);
+            o.y = ((uint32_t)v[2][w] >> 16) | ((uint32_t)v[3][w] & 0xFFFF0000u);
+        } else {
+            o.x = ((uint32_t)v[0][w] & 0xFFFFu) | ((uint32_t)v[1][w] << 16);
+            o.y = ((uint32_t)v[2][w] & 0xFFFFu) | ((uint32_t)v[3][w] << 16);
+        }
+        return o;
+    };
+    auto store = [&](int buf, const i32x4 (&vg)[4], const i32x4 (&vx)[4]) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            const int ch = cv * 8 + e;
-            *(uint16_t *)(lds[buf][0] + ch * kRow + px * 2) = (uint16_t)(gg[e >> 1] >> (16 * (e & 1)));
-            *(uint16_t *)(lds[buf][1] + ch * kRow + px * 2) = (uint16_t)(xx[e >> 1] >> (16 * (e & 1)));
+            const int off = (cv * 8 + e) * kRow + pq * 8;
+            *(uint2 *)(lds[buf][0] + off) = pack(vg, e);
+            *(uint2 *)(lds[buf][1] + off) = pack(vx, e);
+        }
+        if (bias) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    bsum[e] += h16_to_f32<BF16>(((uint32_t)vg[j][e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
         }
     };
     f32x4 acc[2][2];
@@ -231,26 +276,35 @@ __global__ __launch_bounds__(kThreads) void k_wgrad16(const uint16_t *__restrict
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint4 vg[2], vx[2];
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int ks = 0; ks < kPx / 32; ++ks) {
+            const int foff = ks * 64 + (lane >> 4) * 16;   // this lane's 8 pixels
+            short8 af[2], bf[2];
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+                af[mi] = *(const short8 *)(lds[buf][0] + (wm * 32 + mi * 16 + (lane & 15)) * kRow + foff);
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+                bf[ni] = *(const short8 *)(lds[buf][1] + (wn * 32 + ni * 16 + (lane & 15)) * kRow + foff);
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
+        }
+    };
+    // two chunks in flight: register slot d holds chunk c (d = c & 1) until its store,
+    // then receives chunk c + 2; LDS buffer d is rewritten two chunks after it was
+    // read, and every thread passes the barrier in between
+    i32x4 vg[2][4], vx[2][4];
     load(0, vg[0], vx[0]);
     load(1, vg[1], vx[1]);
-    const int foff = (lane >> 4) * 16;            // this lane's 8 pixels within the chunk
     auto step = [&](auto dc, int cc) {
         constexpr int d = decltype(dc)::value;
         store(d, vg[d], vx[d]);
         __syncthreads();
-        load(cc + 2, vg[d], vx[d]);
-        short8 af[2], bf[2];
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-            af[mi] = *(const short8 *)(lds[d][0] + (wm * 32 + mi * 16 + (lane & 15)) * kRow + foff);
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-            bf[ni] = *(const short8 *)(lds[d][1] + (wn * 32 + ni * 16 + (lane & 15)) * kRow + foff);
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
+        load(cc + 2, vg[d], vx[d]);              // past the range: zeros, never used
+        compute(d);
     };
     // whole pairs of chunks in the loop (no exit inside it), then the odd last chunk
     int c = 0;
@@ -272,29 +326,16 @@ __global__ __launch_bounds__(kThreads) void k_wgrad16(const uint16_t *__restrict
                 unsafeAtomicAdd(&dw[((size_t)co * taps + tap) * G.cin + ci], acc[mi][ni][i]);
             }
         }
-}
-
-// db[co] += sum_p G[p][co]: a workgroup sums kBgPx pixels; thread = (channel vector,
-// pixel group)
-constexpr int kBgPx = 256;
-
-template <bool BF16>
-__global__ __launch_bounds__(kThreads) void k_bias_grad16(const uint4 *__restrict__ g, int npix,
-                                                          int vpp, float *__restrict__ db)
-{
-    const int groups = kThreads / vpp;            // pixel groups per workgroup
-    const int v = threadIdx.x % vpp, grp = threadIdx.x / vpp;
-    if (grp >= groups) return;
-    const int p0 = blockIdx.x * kBgPx;
-    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int p = p0 + grp; p < min(npix, p0 + kBgPx); p += groups) {
-        const uint4 q = g[(size_t)p * vpp + v];
-        const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+    if (bias) {
+        // the 32 lanes of one channel vector (one half of the wave) hold its pixel quads
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s[e] += h16_to_f32<BF16>((w4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int m = 1; m < 32; m <<= 1) bsum[e] += __shfl_xor(bsum[e], m, 64);
+        if (pq == 0)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) unsafeAtomicAdd(&db[co0 + cv * 8 + e], bsum[e]);
     }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) unsafeAtomicAdd(&db[v * 8 + e], s[e]);
 }
 
 // ---------------------------------------------------------------- RMSprop
@@ -430,17 +471,8 @@ hipError_t launch_conv_weight_grad(const uint16_t *x, const uint16_t *g, float *
     G.x_bytes = (int)((size_t)fwd.n * fwd.hin * fwd.win * fwd.cin * 2);
     G.g_bytes = (int)((size_t)G.npix * fwd.cout * 2);
     const unsigned grid = (unsigned)((fwd.cout / 64) * ((fwd.cin + 63) / 64) * G.k * G.k * G.splits);
-    if (bf16) hipLaunchKernelGGL(k_wgrad16<true>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, G);
-    else hipLaunchKernelGGL(k_wgrad16<false>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, G);
-    if (db) {
-        const unsigned bgrid = (unsigned)((G.npix + kBgPx - 1) / kBgPx);
-        if (bf16)
-            hipLaunchKernelGGL(k_bias_grad16<true>, dim3(bgrid), dim3(kThreads), 0, s, (const uint4 *)g,
-                               G.npix, fwd.cout / 8, db);
-        else
-            hipLaunchKernelGGL(k_bias_grad16<false>, dim3(bgrid), dim3(kThreads), 0, s, (const uint4 *)g,
-                               G.npix, fwd.cout / 8, db);
-    }
+    if (bf16) hipLaunchKernelGGL(k_wgrad16<true>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, db, G);
+    else hipLaunchKernelGGL(k_wgrad16<false>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, db, G);
     return hipGetLastError();
 }
 

@@ -139,17 +139,21 @@ def test_conv_input_grad_matches_torch(R, k, s, cin, cout, h, w):
     assert max_abs_rel(got, want) <= 2e-2
 
 
-@pytest.mark.parametrize("k,s,cin,cout,h,w", [(3, 1, 64, 64, 16, 32), (3, 2, 32, 64, 64, 128),
-                                              (1, 2, 128, 256, 16, 16), (3, 2, 256, 64, 8, 16)])
-def test_conv_weight_grad_matches_torch(R, k, s, cin, cout, h, w):
+@pytest.mark.parametrize("k,s,cin,cout,h,w,n", [(3, 1, 64, 64, 16, 32, 1), (3, 2, 32, 64, 64, 128, 1),
+                                                (1, 2, 128, 256, 16, 16, 1), (3, 2, 256, 64, 8, 16, 1),
+                                                (3, 1, 64, 64, 6, 6, 3), (3, 1, 64, 128, 8, 40, 3),
+                                                (3, 1, 64, 64, 24, 56, 1)])
+def test_conv_weight_grad_matches_torch(R, k, s, cin, cout, h, w, n):
     """Weight and bias gradients against torch's conv2d_weight in float64 on the same bf16
     values: products of bf16 values are exact in fp32, so only the summation order
-    differs (norm-wise 1e-4), added onto the existing accumulator."""
+    differs (norm-wise 1e-4), added onto the existing accumulator. The last three cases
+    are ragged: four-pixel groups that cross rows and images (6 x 6 maps), a partial
+    last 128-pixel chunk (960 pixels), and a second, partial 1024-pixel range (1344)."""
     from torch.nn.grad import conv2d_weight
     bc, _ = R
-    r = synth.rng(540 + k * s + cin)
-    x = synth.to_storage_bits(synth.normal(r, (1, cin, h, w)), "bf16")
-    g = synth.to_storage_bits(synth.normal(r, (1, cout, h // s, w // s)), "bf16")
+    r = synth.rng(540 + k * s + cin + 7 * n + h)
+    x = synth.to_storage_bits(synth.normal(r, (n, cin, h, w)), "bf16")
+    g = synth.to_storage_bits(synth.normal(r, (n, cout, h // s, w // s)), "bf16")
     want = conv2d_weight(torch.from_numpy(oracle.value(x, "bf16")), (cout, cin, k, k),
                          torch.from_numpy(oracle.value(g, "bf16")), stride=s, padding=k // 2).numpy()
     want_b = oracle.value(g, "bf16").sum(axis=(0, 2, 3))
