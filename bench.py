@@ -156,7 +156,9 @@ def gather_scatter(torch, bc, dev):
     Algorithmic bytes: gather reads and writes every halo tile element once, scatter
     reads and writes every block element once. 'warm': graph of 10 launches (inputs
     can stay in the 256 MB last-level cache); 'cold': each launch follows a 512 MiB
-    read that evicts the caches (graph-differenced, see below)."""
+    read that evicts the caches (graph-differenced, see below). 'plain_copy': torch's
+    contiguous device copy of the gather's byte count, timed the same way: what one
+    launch can move at this size."""
     import numpy as np
 
     import synth
@@ -166,6 +168,9 @@ def gather_scatter(torch, bc, dev):
     idx = torch.empty(128, dtype=torch.int32, device=dev)
     cnt = torch.empty(1, dtype=torch.int32, device=dev)
     bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
+    idx_all = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt_all = torch.empty(1, dtype=torch.int32, device=dev)
+    bc.bc_build_block_index(torch.ones((1, 8, 16), dtype=torch.uint8, device=dev), 1, (8, 16), idx_all, cnt_all)
     flush = torch.ones((4096, 32768), dtype=torch.float32, device=dev)   # 512 MiB
     flush_out = torch.empty(4096, dtype=torch.float32, device=dev)
     out = {}
@@ -174,12 +179,28 @@ def gather_scatter(torch, bc, dev):
         packed = torch.empty((128, 34, 34, c), dtype=torch.bfloat16, device=dev)
         blocks = torch.randn((128, 32, 32, c), device=dev).to(torch.bfloat16)
         dst = torch.empty_like(x)
+        # the ceiling at this size: torch's device copy of the gather's bytes (one
+        # contiguous read and write of the active tiles' size)
+        csrc = torch.empty(n_act * 34 * 34 * c, dtype=torch.bfloat16, device=dev).normal_()
+        cdst = torch.empty_like(csrc)
         ops = {
             "gather": (lambda: bc.bc_gather_halo(x, bc.BC_NHWC, (8, 16), (3, 3, 1, 1, 0), 0.0, idx, cnt, packed),
                        2 * n_act * 34 * 34 * c * 2),
             "scatter": (lambda: bc.bc_scatter_blocks(blocks, idx, cnt, (8, 16), dst, bc.BC_NHWC),
                         2 * n_act * 32 * 32 * c * 2),
+            "plain_copy": (lambda: cdst.copy_(csrc), 2 * n_act * 34 * 34 * c * 2),
         }
+        if c == 256:
+            # every block (150 MB moved): the kernels' rate where launch latency is small
+            asrc = torch.empty(128 * 34 * 34 * c, dtype=torch.bfloat16, device=dev).normal_()
+            adst = torch.empty_like(asrc)
+            ops["gather_all_blocks"] = (
+                lambda: bc.bc_gather_halo(x, bc.BC_NHWC, (8, 16), (3, 3, 1, 1, 0), 0.0, idx_all, cnt_all, packed),
+                2 * 128 * 34 * 34 * c * 2)
+            ops["scatter_all_blocks"] = (
+                lambda: bc.bc_scatter_blocks(blocks, idx_all, cnt_all, (8, 16), dst, bc.BC_NHWC),
+                2 * 128 * 32 * 32 * c * 2)
+            ops["plain_copy_all_blocks"] = (lambda: adst.copy_(asrc), 2 * 128 * 34 * 34 * c * 2)
         for name, (fn, nbytes) in ops.items():
             fn()
             torch.cuda.synchronize()
