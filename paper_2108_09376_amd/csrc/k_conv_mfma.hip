@@ -1061,29 +1061,38 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 // and K split over every ResNet-50 layer of a 2048x1024 frame with 30 % of the blocks
 // active: 64-row tiles are fastest everywhere (at these sizes the kernel is bound by
 // latency and occupancy, and 64x64 tiles keep the most workgroups resident); 128-wide N
-// tiles pay off for 1x1 layers with blocks of 256 or more pixels (the stride-4 and
-// stride-8 maps, many tiles per block) and Cout a multiple of 128; splitting K in two pays off
-// when a full frame has at most 256 tiles (the stride-32 layers) and for 3x3 layers
-// with 512 or more input channels and 513 to 2048 tiles (where nine-tap stages do not
-// apply).
+// tiles pay off for 1x1 layers with Cout a multiple of 128 and blocks of 1024 or more
+// pixels (the stride-4 maps), or blocks of 256 pixels (stride 8) with Cout >= 512 (with
+// fewer output channels the halved tile count costs more: a same-process A/B of whole
+// ResNet-50 frames, 0.6446 -> 0.6330 ms at 30 % active, 0.4699 -> 0.4602 at 10 %);
+// splitting K in two pays off when a full frame has at most 256 tiles (the stride-32
+// layers) and for 3x3 layers with 512 or more input channels and 513 to 2048 tiles
+// (where nine-tap stages do not apply); stride-32 1x1 layers with 16 or more chunks
+// split K in three (0.6410 -> 0.6384 ms at 30 %, no cost at 50 or 100 %; three slices
+// of the nine-tap 3x3 layers gain at 10-30 % but lose 2 % at 50-100 %, where their
+// workgroups outnumber the CUs).
 // Other forms take the largest tile with >= 2048 workgroups on a full frame. The choice
 // depends on the layer's shape only, never on the active count, so an active block's
 // result does not depend on which other blocks are active.
 bool choose_plan(const LayerGeom &g, Plan &best)
 {
     if ((g.kh == 1 || g.kh == 3) && g.cin % 8 == 0) {
-        const int bn = (g.kh == 1 && g.cout % 128 == 0 && g.bh * g.bw >= 256) ? 128 : 64;
+        const int bpx = g.bh * g.bw;
+        const int bn = (g.kh == 1 && g.cout % 128 == 0 && (bpx >= 1024 || (bpx >= 256 && g.cout >= 512)))
+                           ? 128 : 64;
         if (make_plan(g, 64, bn, best) || make_plan(g, 64, 64, best)) {
             MfmaArgs &a = best.a;
             const int nchunk = (g.cin + BK - 1) / BK;
             const unsigned tiles = best.grid;
-            // split K in two for few tiles with a long K, and for 3x3 layers with at least
-            // 512 input channels (sixteen chunks of nine taps per tile otherwise) whose
-            // tiles are too many for nine-tap stages
+            // split K in two for few tiles with a long K (three for 1x1 layers with 16 or
+            // more chunks), and for 3x3 layers with at least 512 input channels (sixteen
+            // chunks of nine taps per tile otherwise) whose tiles are too many for nine-tap
+            // stages
             const bool split = (tiles <= 256 && nchunk >= 8) ||
                                (g.kh == 3 && nchunk >= 16 && tiles > 512 && tiles <= 2048);
             if (best.BM == 64 && best.BN == 64 && split && tiles <= (unsigned)kMaxSplitTiles) {
-                a.cps = (nchunk + 1) / 2;
+                const int ns = (g.kh == 1 && tiles <= 256 && nchunk >= 16) ? 3 : 2;
+                a.cps = (nchunk + ns - 1) / ns;
                 a.ksplit = (nchunk + a.cps - 1) / a.cps;
                 best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);
                 best.grid = tiles * a.ksplit;

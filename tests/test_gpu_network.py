@@ -216,7 +216,7 @@ FULL = [
     (64, 256, 256, 512, 8, 16, 1, 1, True),      # 4096 full-frame tiles: persistent tile walk
     (128, 512, 256, 512, 8, 16, 1, 2, False),    # stride-2 1x1 with 4096 full-frame tiles
     (512, 512, 32, 64, 8, 16, 3, 1, False),      # stride-32 3x3: K split over two workgroups
-    (2048, 512, 32, 64, 8, 16, 1, 1, False),     # stride-32 1x1: K split over two workgroups
+    (2048, 512, 32, 64, 8, 16, 1, 1, False),     # stride-32 1x1: K split over three workgroups
 ]
 
 
