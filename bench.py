@@ -725,8 +725,8 @@ def main():
         else:
             net.frame(x, sparse=True)
 
-    def time_frames(frac, steps, warmup):
-        net.set_mask(masks_for(frac))
+    def time_frames(frac, steps, warmup, mask=None):
+        net.set_mask(masks_for(frac) if mask is None else mask)
         for _ in range(warmup):
             step()
         torch.cuda.synchronize()
@@ -745,6 +745,35 @@ def main():
     for f in [float(v) for v in args.sweep.split(",") if v.strip()]:
         sweep[f"{f:g}"] = round(time_frames(f, max(10, args.steps // 2), 3), 4)
     sweep[f"{args.frac:g}"] = round(ms, 4)
+
+    # Floors of the frame. Chain: one active block (the grid's centre), every layer still
+    # launched. Launches: as many dependent minimal kernels (a one-element add) as the
+    # frame launches (index build + one per layer), captured in one graph.
+    import numpy as np
+    one = np.zeros((1, gh, gw), np.uint8)
+    one[0, gh // 2, gw // 2] = 1
+    one_block_ms = time_frames(0.0, max(10, args.steps // 2), 3, mask=one)
+    n_launch = 1 + len(net.layers)
+    tick = torch.zeros(1, device=dev)
+    lg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(lg):
+        for _ in range(n_launch):
+            tick.add_(1.0)
+    lg.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        lg.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    launch_floor_ms = e0.elapsed_time(e1) / 10
+    del lg
+    floors = {"one_active_block_ms": round(one_block_ms, 4),
+              "dependent_launches_per_frame": n_launch,
+              "launch_floor_ms": round(launch_floor_ms, 4),
+              "launch_floor_us_per_launch": round(launch_floor_ms * 1e3 / n_launch, 3),
+              "roofline_frac_at_launch_floor": round(flops / (launch_floor_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
 
     out = {
         "metric": "effective TFLOP/s on active blocks + ms/frame at 2048x1024, 30% active",
@@ -765,6 +794,7 @@ def main():
                    "batch": 1, "hip_graph": graph is not None},
         "conv_gflop_per_frame": round(flops / 1e9, 3),
         "frame_ms_by_active_fraction": sweep,
+        "frame_floors": floors,
         "roofline": {"bound": "mfma", "kernel": "sparse conv (k_conv_mfma*, all 53 launches of a frame)",
                      "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
