@@ -98,6 +98,7 @@ struct MfmaArgs {
     FastDiv f_hrhc, f_hc, f_rbw, f_bw;  // divisions by HR*HC, HC, R*bw, bw
     int ksplit, cps;                    // K slices per tile, 32-channel chunks per slice
     int tiles_full;                     // tiles (incl. K slices) of a full frame
+    int slots;                          // stem form: workgroups resident on the device
 };
 
 template <bool BF16>
@@ -803,18 +804,29 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
     extern __shared__ __align__(16) uint8_t smem[];
 
     __shared__ TileBlocks tb;
-    const int mt = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
+    const int grp = blockIdx.x / a.ntn, nt = blockIdx.x - (blockIdx.x / a.ntn) * a.ntn;
     const int n0 = nt * BN;
-    if (!load_tile_blocks(a, mt, tb)) return;
+    // A workgroup stages the N tile's weights once and computes `per` consecutive M
+    // tiles with them, `per` chosen so the active tiles fill at most the resident
+    // workgroups. A tile's result does not depend on which workgroup computes it.
+    const int cnt = a.count ? *a.count : a.total_blocks;
+    const int act = (a.P == 1) ? cnt * a.tpb : (cnt + a.P - 1) / a.P;   // active M tiles
+    const int slots = max(1, a.slots);
+    const int per = max(1, (act * a.ntn + slots - 1) / slots);
+    const int mt0 = grp * per;
+    if (mt0 >= act) return;                  // uniform
+    load_tile_blocks(a, mt0, tb);            // active: mt0 < act
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int hcp = a.rowpitch;              // pixels per LDS halo row (>= (bw-1)*S + 32/CP)
     const int kwc = KS * a.cin;              // weight values per kernel row
     const int wvals = BN * KS * kwc;         // weights of this N tile
-    uint8_t *sA = smem;                                              // [P][HR][hcp][CP]
+    // LDS: rearranged weights, then the halo and the raw weights (the epilogue's scratch
+    // reuses the halo and raw-weight space)
+    uint16_t *sB = (uint16_t *)smem;                                 // [KS][BN][BKP]
+    uint8_t *sA = smem + KS * BN * BKP * 2;                          // [P][HR][hcp][CP]
     const int a_bytes = ((a.P * a.HR * hcp * CP * 2) + 15) & ~15;
-    uint16_t *sB = (uint16_t *)(smem + a_bytes);                     // [KS][BN][BKP]
-    uint16_t *sW = sB + KS * BN * BKP;                               // raw [BN][KS*kwc]
+    uint16_t *sW = (uint16_t *)(sA + a_bytes);                       // raw [BN][KS*kwc]
 
     // raw weights of the N tile: one contiguous run, 16-byte requests
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
@@ -879,17 +891,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
             if (v < nvec) *(uint4 *)((uint8_t *)sW + v * 16) = wv[u];
         }
     }
-    Epilogue<BF16, BM, BN> epi;
-    epi.prefetch(a, tb, n0);
-
-    // halo pixels with CP channels each (zeros outside the image, past Cin, in the tail)
-    halo_store(0, hv);
-    for (int e0 = SPT * kThreads; e0 < npix; e0 += SPT * kThreads) {
-        halo_batch(e0, hv);
-        halo_store(e0, hv);
-    }
     __syncthreads();
     // rearrange weights: B[i][n][kk] = W[n][i][j][c] with kk = j*CP + c, zero elsewhere
+    // (sB is complete after the barrier that follows the first tile's halo)
     {
         const int n = tid >> 2, kq = tid & 3;
         const uint16_t *src = sW + n * KS * kwc;
@@ -911,7 +915,6 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
             *(uint4 *)(sB + (i * BN + n) * BKP + kq * 8) = make_uint4(w2[0], w2[1], w2[2], w2[3]);
         }
     }
-    __syncthreads();
 
     const int rbw = a.R * a.bw;
     int aoffs[MI];
@@ -923,35 +926,51 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
         const int pr = fdiv(local, a.f_bw), pc = local - pr * a.bw;
         aoffs[mi] = ((p * a.HR + pr * S) * hcp + pc * S + (lane >> 4) * PPK) * CP * 2;
     }
-    f32x4 acc[MI][NI];
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int i = 0; i < KS; ++i) {
-        short8 af[MI], bf[NI];
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi) {
-            const uint8_t *src = sA + aoffs[mi] + i * hcp * CP * 2;
-            if constexpr (CP == 8 || S % 2 == 0) {
-                af[mi] = *(const short8 *)src;                  // 16-byte aligned
-            } else {
-                const uint2 lo = *(const uint2 *)src, hi = *(const uint2 *)(src + 8);
-                af[mi] = __builtin_bit_cast(short8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-            }
+    for (int t = 0;;) {
+        Epilogue<BF16, BM, BN> epi;
+        epi.prefetch(a, tb, n0);
+        // halo pixels with CP channels each (zeros outside the image, past Cin, in the tail)
+        halo_store(0, hv);
+        for (int e0 = SPT * kThreads; e0 < npix; e0 += SPT * kThreads) {
+            halo_batch(e0, hv);
+            halo_store(e0, hv);
         }
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
-            bf[ni] = *(const short8 *)(sB + (i * BN + wn * WN + ni * 16 + (lane & 15)) * BKP +
-                                       (lane >> 4) * 8);
+        __syncthreads();
+        f32x4 acc[MI][NI];
 #pragma unroll
         for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
+            for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+            short8 af[MI], bf[NI];
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi) {
+                const uint8_t *src = sA + aoffs[mi] + i * hcp * CP * 2;
+                if constexpr (CP == 8 || S % 2 == 0) {
+                    af[mi] = *(const short8 *)src;                  // 16-byte aligned
+                } else {
+                    const uint2 lo = *(const uint2 *)src, hi = *(const uint2 *)(src + 8);
+                    af[mi] = __builtin_bit_cast(short8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+                }
+            }
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+                bf[ni] = *(const short8 *)(sB + (i * BN + wn * WN + ni * 16 + (lane & 15)) * BKP +
+                                           (lane >> 4) * 8);
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma<BF16>(af[mi], bf[ni], acc[mi][ni]);
+        }
+        epi.finish(a, acc, sA, n0);
+        if (++t == per || mt0 + t >= act) break;
+        // the next tile: its blocks (the barrier inside also keeps the halo stores below
+        // behind every wave's epilogue reads of the scratch), then its first halo batch
+        load_tile_blocks(a, mt0 + t, tb);
+        halo_batch(0, hv);
     }
-    epi.finish(a, acc, smem, n0);
 }
 
 // ------------------------------------------------------------------ planning
@@ -972,6 +991,21 @@ struct Plan {
 constexpr size_t kMaxLdsPipe = 159 * 1024;   // 160 KB less room for static shared memory
 
 size_t epi_lds(int BM) { return (size_t)4 * (BM / 2) * EPITCH * sizeof(float); }
+
+// Compute units of the current device (cached per device; 256 if the query fails).
+int device_cus()
+{
+    static int cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] <= 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
 size_t round16(size_t v) { return (v + 15) & ~(size_t)15; }
 
 // LDS of the pipelined form: double buffers of the halo and of the weight slices (SG per
@@ -1020,10 +1054,11 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
         a.rowpitch = (((g.bw - 1) * S + 32 / CP) + 1) & ~1;   // pixels per LDS halo row, even
         a.nslot = 0;
         const size_t abytes = ((size_t)a.P * a.HR * a.rowpitch * CP * 2 + 15) & ~(size_t)15;
-        const size_t main = abytes + (size_t)KS * BN * 40 * 2 +
-                            (((size_t)BN * KS * KS * g.cin * 2 + 15) & ~(size_t)15);
-        pl.lds = main > epi_lds(BM) ? main : epi_lds(BM);
+        const size_t staged = abytes + (((size_t)BN * KS * KS * g.cin * 2 + 15) & ~(size_t)15);
+        pl.lds = (size_t)KS * BN * 40 * 2 + (staged > epi_lds(BM) ? staged : epi_lds(BM));
         if (pl.lds > kMaxLdsPipe) return false;
+        const int per_cu = (int)((160 * 1024) / pl.lds);
+        a.slots = device_cus() * (per_cu < 1 ? 1 : per_cu > 4 ? 4 : per_cu);
     } else {
         if (KS == 1) {
             a.HR = a.R;

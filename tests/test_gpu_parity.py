@@ -164,6 +164,8 @@ CASES = [
     (3, 64, 32, 64, 2, 4, 1, 1, True, False, 0.5),      # 1x1 with Cin=3 (stem form)
     (5, 64, 32, 64, 2, 4, 3, 1, True, True, 0.5),       # Cin=5: 8 padded channels per pixel
     (3, 64, 64, 64, 2, 2, 7, 1, True, False, 0.5),      # 7x7/1 stem form (unaligned rows)
+    (3, 64, 512, 1024, 16, 32, 7, 2, True, False, 0.9), # stem form, more active tiles than
+                                                        # resident workgroups: several each
 ]
 
 
