@@ -25,7 +25,12 @@ __device__ __forceinline__ void block_of(const LayerGeom &g, int k, int &img, in
     gx = rem - gy * g.gw;
 }
 
-// grid.x = total_blocks * parts; each workgroup covers kThreads (pixel, 8-channel) pairs
+// grid.x = total_blocks * parts; each workgroup covers kThreads (pixel, 8-channel) pairs.
+// KS > 0: a KS x KS window known at compile time; every tap's load is issued before any
+// is used (coordinates clamped into the image, so every address is valid, and taps
+// outside the image replaced by -inf afterwards), one memory round trip per thread.
+// KS = 0: any window, taps in a loop.
+template <int KS>
 __global__ __launch_bounds__(kThreads) void k_maxpool_nhwc16(const uint16_t *__restrict__ x,
                                                              uint16_t *__restrict__ y,
                                                              LayerGeom g, int parts, int bf16)
@@ -45,19 +50,38 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_nhwc16(const uint16_t *__r
     float m[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) m[q] = -__builtin_huge_valf();
-    for (int i = 0; i < g.kh; ++i) {
-        const int iy = oy * g.stride - g.pad + i;
-        if (iy < 0 || iy >= g.hin) continue;
-        for (int j = 0; j < g.kw; ++j) {
-            const int ix = ox * g.stride - g.pad + j;
-            if (ix < 0 || ix >= g.win) continue;
-            const uint4 v = *(const uint4 *)(x + (((size_t)img * g.hin + iy) * g.win + ix) * g.cin +
-                                             c8 * 8);
-            const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+    auto take = [&](const uint4 v) {
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                m[2 * q] = fmaxf(m[2 * q], h16_to_f32((uint16_t)(w4[q] & 0xFFFFu), bf16));
-                m[2 * q + 1] = fmaxf(m[2 * q + 1], h16_to_f32((uint16_t)(w4[q] >> 16), bf16));
+        for (int q = 0; q < 4; ++q) {
+            m[2 * q] = fmaxf(m[2 * q], h16_to_f32((uint16_t)(w4[q] & 0xFFFFu), bf16));
+            m[2 * q + 1] = fmaxf(m[2 * q + 1], h16_to_f32((uint16_t)(w4[q] >> 16), bf16));
+        }
+    };
+    const uint16_t *xi = x + (size_t)img * g.hin * g.win * g.cin + c8 * 8;
+    if constexpr (KS > 0) {
+        uint4 v[KS * KS];
+        bool in[KS * KS];
+#pragma unroll
+        for (int i = 0; i < KS; ++i)
+#pragma unroll
+            for (int j = 0; j < KS; ++j) {
+                const int iy = oy * g.stride - g.pad + i, ix = ox * g.stride - g.pad + j;
+                in[i * KS + j] = iy >= 0 && iy < g.hin && ix >= 0 && ix < g.win;
+                const int cy = min(max(iy, 0), g.hin - 1), cx = min(max(ix, 0), g.win - 1);
+                v[i * KS + j] = *(const uint4 *)(xi + ((size_t)cy * g.win + cx) * g.cin);
+            }
+#pragma unroll
+        for (int t = 0; t < KS * KS; ++t)
+            if (in[t]) take(v[t]);
+    } else {
+        for (int i = 0; i < g.kh; ++i) {
+            const int iy = oy * g.stride - g.pad + i;
+            if (iy < 0 || iy >= g.hin) continue;
+            for (int j = 0; j < g.kw; ++j) {
+                const int ix = ox * g.stride - g.pad + j;
+                if (ix < 0 || ix >= g.win) continue;
+                take(*(const uint4 *)(xi + ((size_t)iy * g.win + ix) * g.cin));
             }
         }
     }
@@ -115,8 +139,12 @@ hipError_t launch_maxpool_nhwc16(const uint16_t *x, uint16_t *y, Half16 fmt, con
 {
     const int work = g.bh * g.bw * (g.cout / 8);
     const int parts = (work + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL(k_maxpool_nhwc16, dim3((unsigned)g.total_blocks * parts), dim3(kThreads), 0,
-                       s, x, y, g, parts, fmt == Half16::BF16 ? 1 : 0);
+    const dim3 grid((unsigned)g.total_blocks * parts);
+    const int bf = fmt == Half16::BF16 ? 1 : 0;
+    if (g.kh == 3 && g.kw == 3)
+        hipLaunchKernelGGL(k_maxpool_nhwc16<3>, grid, dim3(kThreads), 0, s, x, y, g, parts, bf);
+    else
+        hipLaunchKernelGGL(k_maxpool_nhwc16<0>, grid, dim3(kThreads), 0, s, x, y, g, parts, bf);
     return hipGetLastError();
 }
 

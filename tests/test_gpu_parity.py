@@ -267,17 +267,21 @@ def test_conv_active_bits_independent_of_mask(B, case):
 
 # ------------------------------------------------------------------ a6: max pooling
 
-@pytest.mark.parametrize("dtype,nhwc", [("bf16", True), ("f16", True), ("f32", False)])
-def test_maxpool_bit_exact(B, dtype, nhwc):
+@pytest.mark.parametrize("dtype,nhwc,k,s,p", [("bf16", True, 3, 2, 1), ("f16", True, 3, 2, 1),
+                                               ("f32", False, 3, 2, 1), ("bf16", True, 2, 2, 0),
+                                               ("bf16", True, 5, 2, 2)])
+def test_maxpool_bit_exact(B, dtype, nhwc, k, s, p):
+    """The 3x3 window (every tap requested up front, clamped) and other windows (a loop
+    over the taps), border blocks included."""
     r = synth.rng(100)
     c, h, w, gh, gw = 64 if nhwc else 16, 64, 128, 4, 8
     x = synth.to_storage_bits(synth.normal(r, (1, c, h, w)), dtype)
     prev = synth.nan_canaries(r, (1, c, h // 2, w // 2), dtype)
     mask = synth.frac_mask(101, gh, gw, 0.4)
-    want = oracle.sparse_maxpool2d(x, mask, prev, dtype, 3, 2, 1)
+    want = oracle.sparse_maxpool2d(x, mask, prev, dtype, k, s, p)
     idx, cnt, _ = _index(B, mask)
     out = to_dev(prev, dtype, nhwc)
-    B.bc_sparse_maxpool2d((3, 3, 2, 1, 0), to_dev(x, dtype, nhwc), B.BC_NHWC if nhwc else B.BC_NCHW,
+    B.bc_sparse_maxpool2d((k, k, s, p, 0), to_dev(x, dtype, nhwc), B.BC_NHWC if nhwc else B.BC_NCHW,
                           out, (gh, gw), idx, cnt)
     assert np.array_equal(from_dev(out, nhwc), want)
 
