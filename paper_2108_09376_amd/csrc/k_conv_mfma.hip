@@ -48,6 +48,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x3 __attribute__((ext_vector_type(3)));
 
 // Raw buffer resource: no swizzle, 32-bit dword data format; loads at offsets beyond
 // num_records return zeros instead of faulting.
@@ -876,8 +877,59 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
             }
         }
     };
+    // Three channels of 16 bits and an even row width: the two pixels at image x = 2q and
+    // 2q + 1 are 12 contiguous bytes at a 4-byte aligned offset, one 12-byte request
+    // instead of one 2-byte request per pixel and channel. Pairs cover halo columns
+    // -1 .. hcp; columns at or past HC get zeros (as in the per-channel path).
+    const bool pairs = CP == 4 && a.cin == 3 && (a.win & 1) == 0;
+    const int npr = (hcp + 3) >> 1;          // pairs per halo row
+    const int nprs = a.P * a.HR * npr;
+    constexpr int PPT = 3;                   // pairs per thread per batch
+    auto pair_geom = [&](int e, int &row, int &x, int &c0, int &off) {
+        row = e / npr;
+        const int k = e - row * npr;
+        const int p = min(row / a.HR, a.P - 1);
+        const int hy = row - p * a.HR;
+        const int img = tb.img[p];
+        const int ix0 = tb.ox0[p] * S - a.pad;          // image x of halo column 0
+        x = 2 * ((ix0 >> 1) + k);                       // even image x of the pair
+        c0 = x - ix0;                                   // its halo column: 2k or 2k - 1
+        const int iy = tb.oy0[p] * S - a.pad + hy;
+        off = (e < nprs && img >= 0 && iy >= 0 && iy < a.hin && x >= 0 && x < a.win)
+                  ? ((img * a.hin + iy) * a.win + x) * 6
+                  : kOutOfRange;
+    };
+    auto pair_batch = [&](int e0, i32x3 (&v)[PPT]) {
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            int row, x, c0, off;
+            pair_geom(e0 + u * kThreads + tid, row, x, c0, off);
+            asm volatile("" : "+v"(off));
+            v[u] = __builtin_amdgcn_raw_buffer_load_b96(xr, off, 0, 0);
+        }
+    };
+    auto pair_store = [&](int e0, const i32x3 (&v)[PPT]) {
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = e0 + u * kThreads + tid;
+            if (e >= nprs) continue;
+            int row, x, c0, off;
+            pair_geom(e, row, x, c0, off);
+            const uint32_t w0 = (uint32_t)v[u][0], w1 = (uint32_t)v[u][1], w2 = (uint32_t)v[u][2];
+            uint8_t *rp = sA + (size_t)row * hcp * 8;
+            if (c0 >= 0 && c0 < hcp)
+                *(uint2 *)(rp + c0 * 8) = c0 < a.HC ? make_uint2(w0, w1 & 0xFFFFu) : make_uint2(0u, 0u);
+            if (c0 + 1 < hcp)
+                *(uint2 *)(rp + (c0 + 1) * 8) =
+                    c0 + 1 < a.HC ? make_uint2((w1 >> 16) | (w2 << 16), w2 >> 16) : make_uint2(0u, 0u);
+        }
+    };
     uint16_t hv[SPT][CP];
-    halo_batch(0, hv);
+    i32x3 pv[PPT];
+    if (pairs)
+        pair_batch(0, pv);
+    else
+        halo_batch(0, hv);
     for (int v0 = 0; v0 < nvec; v0 += WPT * kThreads) {
         uint4 wv[WPT];
 #pragma unroll
@@ -930,10 +982,18 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
         Epilogue<BF16, BM, BN> epi;
         epi.prefetch(a, tb, n0);
         // halo pixels with CP channels each (zeros outside the image, past Cin, in the tail)
-        halo_store(0, hv);
-        for (int e0 = SPT * kThreads; e0 < npix; e0 += SPT * kThreads) {
-            halo_batch(e0, hv);
-            halo_store(e0, hv);
+        if (pairs) {
+            pair_store(0, pv);
+            for (int e0 = PPT * kThreads; e0 < nprs; e0 += PPT * kThreads) {
+                pair_batch(e0, pv);
+                pair_store(e0, pv);
+            }
+        } else {
+            halo_store(0, hv);
+            for (int e0 = SPT * kThreads; e0 < npix; e0 += SPT * kThreads) {
+                halo_batch(e0, hv);
+                halo_store(e0, hv);
+            }
         }
         __syncthreads();
         f32x4 acc[MI][NI];
@@ -969,7 +1029,10 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma_stem(MfmaArgs a)
         // the next tile: its blocks (the barrier inside also keeps the halo stores below
         // behind every wave's epilogue reads of the scratch), then its first halo batch
         load_tile_blocks(a, mt0 + t, tb);
-        halo_batch(0, hv);
+        if (pairs)
+            pair_batch(0, pv);
+        else
+            halo_batch(0, hv);
     }
 }
 

@@ -166,6 +166,8 @@ CASES = [
     (3, 64, 64, 64, 2, 2, 7, 1, True, False, 0.5),      # 7x7/1 stem form (unaligned rows)
     (3, 64, 512, 1024, 16, 32, 7, 2, True, False, 0.9), # stem form, more active tiles than
                                                         # resident workgroups: several each
+    (3, 64, 64, 63, 2, 4, 7, 2, True, False, 0.5),      # stem form, odd input width: pixels
+                                                        # staged one channel at a time
 ]
 
 
