@@ -225,6 +225,59 @@ def test_policy_step_validation_codes(B):
     assert B.bc_last_error()
 
 
+def test_training_validation_codes(B):
+    """The policy's update entry points reject bad arguments before enqueuing. Every call
+    here fails a check (the pointers are fakes): none may reach a launch."""
+    lib = B.raw()
+    byref = ctypes.byref
+    # logit gradient into the head's [n][gh][gw][c] map
+    head = B.bc_tensor(1, 64, 8, 16, 1, 1)
+    assert lib.bc_policy_logit_grad(None, FAKE_W, FAKE_RES, FAKE_OUT, head, None) == B.BC_ERR_NULL
+    assert lib.bc_policy_logit_grad(FAKE_IN, FAKE_W, FAKE_RES, FAKE_OUT, B.bc_tensor(1, 64, 8, 16, 1, 0), None) == B.BC_ERR_LAYOUT
+    assert lib.bc_policy_logit_grad(FAKE_IN, FAKE_W, FAKE_RES, FAKE_OUT, B.bc_tensor(1, 64, 8, 16, 0, 1), None) == B.BC_ERR_DTYPE
+    assert lib.bc_policy_logit_grad(FAKE_IN, FAKE_W, FAKE_RES, FAKE_OUT, B.bc_tensor(1, 12, 8, 16, 1, 1), None) == B.BC_ERR_UNSUPPORTED
+    assert lib.bc_policy_logit_grad(FAKE_IN, FAKE_W, FAKE_RES, FAKE_IN + 64, head, None) == B.BC_ERR_ALIAS
+    # gradient combine
+    m = B.bc_tensor(1, 64, 32, 64, 1, 1)
+    assert lib.bc_grad_combine(None, None, None, m, FAKE_OUT, None) == B.BC_ERR_NULL
+    assert lib.bc_grad_combine(FAKE_IN, None, None, m, None, None) == B.BC_ERR_NULL
+    assert lib.bc_grad_combine(FAKE_IN, None, None, B.bc_tensor(1, 64, 32, 64, 0, 1), FAKE_OUT, None) == B.BC_ERR_DTYPE
+    assert lib.bc_grad_combine(FAKE_IN, None, None, B.bc_tensor(1, 64, 32, 64, 1, 0), FAKE_OUT, None) == B.BC_ERR_LAYOUT
+    assert lib.bc_grad_combine(FAKE_IN, FAKE_W, FAKE_RES, m, FAKE_IN + 16, None) == B.BC_ERR_ALIAS   # partial overlap
+    # input gradient: grad_in [n][h][w][cin], grad_out [n][h/s][w/s][cout]
+    gi, go = B.bc_tensor(1, 64, 32, 64, 1, 1), B.bc_tensor(1, 128, 16, 32, 1, 1)
+    c3s2 = B.bc_conv(3, 3, 2, 1, 0)
+    ig = lambda geom=c3s2, o=go, i=gi, out=FAKE_OUT, w=FAKE_W: lib.bc_conv2d_input_grad(
+        None if geom is None else byref(geom), FAKE_IN, o, w, None, out, i, None)
+    assert ig(geom=None) == B.BC_ERR_NULL and ig(w=None) == B.BC_ERR_NULL and ig(out=None) == B.BC_ERR_NULL
+    assert ig(geom=B.bc_conv(5, 5, 2, 2, 0)) == B.BC_ERR_UNSUPPORTED      # 1x1 or 3x3 only
+    assert ig(geom=B.bc_conv(3, 3, 3, 1, 0)) == B.BC_ERR_UNSUPPORTED      # stride 1 or 2
+    assert ig(geom=B.bc_conv(3, 3, 2, 0, 0)) == B.BC_ERR_UNSUPPORTED      # pad k/2
+    assert ig(o=B.bc_tensor(1, 128, 16, 30, 1, 1)) == B.BC_ERR_SHAPE      # not the layer's output
+    assert ig(o=B.bc_tensor(1, 96, 16, 32, 1, 1)) == B.BC_ERR_UNSUPPORTED # cout % 64
+    assert ig(i=B.bc_tensor(1, 32, 32, 64, 1, 1)) == B.BC_ERR_UNSUPPORTED # cin % 64
+    assert ig(i=B.bc_tensor(1, 64, 20, 64, 1, 1), o=B.bc_tensor(1, 128, 10, 32, 1, 1)) == B.BC_ERR_UNSUPPORTED
+    assert ig(o=B.bc_tensor(1, 128, 16, 32, 2, 1)) == B.BC_ERR_DTYPE      # fp16 against bf16
+    assert ig(out=FAKE_IN + 64) == B.BC_ERR_ALIAS
+    # weight gradient (adds into fp32 dW / db)
+    wg = lambda geom=c3s2, i=gi, o=go, dw=FAKE_OUT, db=None: lib.bc_conv2d_weight_grad(
+        None if geom is None else byref(geom), FAKE_IN, i, FAKE_W, o, dw, db, None)
+    assert wg(geom=None) == B.BC_ERR_NULL and wg(dw=None) == B.BC_ERR_NULL
+    assert wg(i=B.bc_tensor(1, 64, 32, 64, 1, 0)) == B.BC_ERR_LAYOUT
+    assert wg(o=B.bc_tensor(1, 128, 17, 32, 1, 1)) == B.BC_ERR_SHAPE
+    assert wg(dw=FAKE_IN + 64) == B.BC_ERR_ALIAS
+    assert wg(db=FAKE_OUT + 64) == B.BC_ERR_ALIAS                         # db inside dW
+    # RMSprop
+    f = ctypes.c_float
+    rp = lambda w=FAKE_IN, v=FAKE_W, g=FAKE_RES, n=1000, w16=None, dt=1: lib.bc_rmsprop_step(
+        w, v, g, ctypes.c_int64(n), f(1e-4), f(0.99), f(1e-8), f(1e-3), w16, dt, None)
+    assert rp(g=None) == B.BC_ERR_NULL
+    assert rp(n=0) == B.BC_ERR_SHAPE and rp(n=(1 << 31) + 1) == B.BC_ERR_SHAPE
+    assert rp(w16=FAKE_OUT, dt=0) == B.BC_ERR_DTYPE
+    assert rp(v=FAKE_IN + 400) == B.BC_ERR_ALIAS and rp(w16=FAKE_RES + 8) == B.BC_ERR_ALIAS
+    assert B.bc_last_error()
+
+
 @no_gpu
 def test_buffer_registry_rules(B):
     lib = B.raw()
