@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 5
+#define BC_ABI_VERSION 6
 
 typedef enum {
     BC_OK = 0,
@@ -414,6 +414,21 @@ bc_status bc_conv2d_weight_grad(const bc_conv *geom, const void *d_in, bc_tensor
 bc_status bc_rmsprop_step(float *d_w, float *d_v, float *d_grad, int64_t count, float lr,
                           float alpha, float eps, float weight_decay, void *d_w16, int32_t dtype,
                           void *stream);
+
+/* One parameter tensor of a multi-tensor RMSprop step: fp32 weights, squared-gradient
+ * average and gradient of `count` elements, and an optional 16-bit copy of the weights. */
+typedef struct { float *w, *v, *grad; void *w16; int64_t count; } bc_param;
+
+/*
+ * bc_rmsprop_step on n tensors (1 <= n <= 64) in one launch, same arithmetic and the
+ * same hyper-parameters for all; `params` is a host array read during the call (its
+ * pointers and sizes travel in the launch's arguments, nothing is allocated). Every
+ * w16 copy has the dtype `dtype`. No two buffers of any tensors may overlap.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE (n or a count out of range), BC_ERR_DTYPE,
+ * BC_ERR_ALIAS, BC_ERR_HIP.
+ */
+bc_status bc_rmsprop_step_many(const bc_param *params, int32_t n, float lr, float alpha, float eps,
+                               float weight_decay, int32_t dtype, void *stream);
 
 /*
  * Block rewards and the policy loss (Section 3.5), per image n of the batch:

@@ -38,6 +38,11 @@ class bc_grid(ctypes.Structure):
     _fields_ = [("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32)]
 
 
+class bc_param(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("v", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("w16", ctypes.c_void_p), ("count", ctypes.c_int64)]
+
+
 class bc_conv(ctypes.Structure):
     _fields_ = [("kh", ctypes.c_int32), ("kw", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
@@ -81,6 +86,7 @@ _sigs = {
     "bc_conv2d_input_grad": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, bc_tensor, _vp], _i32),
     "bc_conv2d_weight_grad": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, _vp, _vp, _vp], _i32),
     "bc_rmsprop_step": ([_vp, _vp, _vp, ctypes.c_int64, _f32, _f32, _f32, _f32, _vp, _i32, _vp], _i32),
+    "bc_rmsprop_step_many": ([ctypes.POINTER(bc_param), _i32, _f32, _f32, _f32, _f32, _i32, _vp], _i32),
     "bc_block_rewards": ([_vp, _vp, _vp, _i32, bc_grid, _f32, _f32, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
 }
 for _name, (_args, _res) in _sigs.items():
@@ -92,7 +98,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 5
+ABI_VERSION = 6
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -311,6 +317,20 @@ def bc_rmsprop_step(w, v, grad, lr, alpha, eps, weight_decay, w16=None, stream=N
     st = _lib.bc_rmsprop_step(_ptr(w), _ptr(v), _ptr(grad), ctypes.c_int64(int(w.numel())), float(lr),
                               float(alpha), float(eps), float(weight_decay), _ptr(w16), dt, _stream(stream))
     _check(st, "bc_rmsprop_step")
+
+
+def bc_rmsprop_step_many(params, lr, alpha, eps, weight_decay, stream=None):
+    """bc_rmsprop_step on every (w, v, grad, w16 or None) of `params` in one launch; the
+    16-bit copies share one dtype."""
+    arr = (bc_param * len(params))()
+    dt = BC_BF16
+    for i, (w, v, grad, w16) in enumerate(params):
+        arr[i] = bc_param(_ptr(w), _ptr(v), _ptr(grad), _ptr(w16), int(w.numel()))
+        if w16 is not None:
+            dt = _dtype_code(w16)
+    st = _lib.bc_rmsprop_step_many(arr, len(params), float(lr), float(alpha), float(eps),
+                                   float(weight_decay), dt, _stream(stream))
+    _check(st, "bc_rmsprop_step_many")
 
 
 def bc_block_rewards(ig, mask, prob, grid, tau, gamma, mu, mavg, reward, cost=None, loss=None,

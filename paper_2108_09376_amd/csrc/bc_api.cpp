@@ -3,6 +3,7 @@
 // before anything is enqueued; kernels are launched on the caller's stream.
 #include <math.h>
 #include <cmath>
+#include <vector>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -828,6 +829,50 @@ bc_status bc_rmsprop_step(float *d_w, float *d_v, float *d_grad, int64_t count, 
         return fail(BC_ERR_ALIAS, "the optimiser's buffers overlap");
     hipError_t e = bc::launch_rmsprop(d_w, d_v, d_grad, (long long)count, lr, alpha, eps, weight_decay,
                                       d_w16, dtype == BC_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "rmsprop launch");
+    return ok();
+}
+
+bc_status bc_rmsprop_step_many(const bc_param *params, int32_t n, float lr, float alpha, float eps,
+                               float weight_decay, int32_t dtype, void *stream)
+{
+    if (!params) return fail(BC_ERR_NULL, "params is required");
+    if (n < 1 || n > bc::kMaxParams) return fail(BC_ERR_SHAPE, "n outside 1..%d", bc::kMaxParams);
+    bc::RmspropMany m{};
+    m.n = n;
+    bool any16 = false;
+    long long blocks = 0;
+    for (int t = 0; t < n; ++t) {
+        const bc_param &p = params[t];
+        if (!p.w || !p.v || !p.grad) return fail(BC_ERR_NULL, "params[%d]: w, v and grad are required", t);
+        if (p.count <= 0 || p.count > ((int64_t)1 << 31)) return fail(BC_ERR_SHAPE, "params[%d]: count outside 1..2^31", t);
+        any16 = any16 || p.w16;
+        m.w[t] = p.w;
+        m.v[t] = p.v;
+        m.grad[t] = p.grad;
+        m.w16[t] = (uint16_t *)p.w16;
+        m.count[t] = p.count;
+        m.first[t] = (int)blocks;
+        blocks += (p.count + 255) / 256;
+    }
+    m.first[n] = (int)blocks;
+    if (any16 && dtype != BC_BF16 && dtype != BC_F16) return fail(BC_ERR_DTYPE, "the copies must be bf16 or f16");
+    // every buffer of every tensor against every other
+    struct Span { const void *p; size_t b; };
+    std::vector<Span> spans;
+    for (int t = 0; t < n; ++t) {
+        const size_t b = (size_t)params[t].count * 4;
+        spans.push_back({params[t].w, b});
+        spans.push_back({params[t].v, b});
+        spans.push_back({params[t].grad, b});
+        if (params[t].w16) spans.push_back({params[t].w16, (size_t)params[t].count * 2});
+    }
+    for (size_t i = 0; i < spans.size(); ++i)
+        for (size_t j = i + 1; j < spans.size(); ++j)
+            if (overlap(spans[i].p, spans[i].b, spans[j].p, spans[j].b))
+                return fail(BC_ERR_ALIAS, "the optimiser's buffers overlap");
+    hipError_t e = bc::launch_rmsprop_many(m, lr, alpha, eps, weight_decay, dtype == BC_BF16,
+                                           (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "rmsprop launch");
     return ok();
 }

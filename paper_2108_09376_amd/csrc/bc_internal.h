@@ -89,6 +89,18 @@ hipError_t launch_conv_input_grad(const uint16_t *grad_out, const uint16_t *w, c
                                   hipStream_t s, const char **why);
 hipError_t launch_conv_weight_grad(const uint16_t *x, const uint16_t *g, float *dw, float *db,
                                    const LayerGeom &fwd, bool bf16, hipStream_t s);
+// Multi-tensor RMSprop: up to kMaxParams tensors; first[t] is the first workgroup of
+// tensor t (first[n] = the grid), each workgroup covering 256 elements.
+constexpr int kMaxParams = 64;
+struct RmspropMany {
+    float *w[kMaxParams], *v[kMaxParams], *grad[kMaxParams];
+    uint16_t *w16[kMaxParams];
+    long long count[kMaxParams];
+    int first[kMaxParams + 1];
+    int n;
+};
+hipError_t launch_rmsprop_many(const RmspropMany &m, float lr, float alpha, float eps, float wd,
+                               bool bf16, hipStream_t s);
 hipError_t launch_rmsprop(float *w, float *v, float *grad, long long count, float lr, float alpha,
                           float eps, float wd, void *w16, bool bf16, hipStream_t s);
 

@@ -26,7 +26,8 @@
 //    channel and workgroup;
 //  * RMSprop (PyTorch's definition, no momentum): g' = g + wd w; v = alpha v +
 //    (1 - alpha) g'^2; w -= lr g' / (sqrt(v) + eps); the gradient is reset to 0 and the
-//    16-bit copy of w rewritten (round to nearest even).
+//    16-bit copy of w rewritten (round to nearest even); for one tensor, or for up to
+//    kMaxParams tensors in one launch (their pointers and sizes in the kernel arguments).
 #include <mutex>
 #include <type_traits>
 
@@ -358,6 +359,29 @@ __global__ __launch_bounds__(kThreads) void k_rmsprop(float *__restrict__ w, flo
     if (w16) w16[t] = (uint16_t)f32_to_h16<BF16>(wn);
 }
 
+// Several tensors in one launch: workgroup b belongs to the tensor t with
+// first[t] <= b < first[t + 1] (a uniform scan over at most kMaxParams entries of the
+// kernel arguments), element (b - first[t]) * kThreads + thread of that tensor.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void k_rmsprop_many(RmspropMany m, float lr, float alpha,
+                                                           float eps, float wd)
+{
+    const int b = blockIdx.x;
+    int t = 0;
+    while (t + 1 < m.n && m.first[t + 1] <= b) ++t;
+    const long long i = (long long)(b - m.first[t]) * kThreads + threadIdx.x;
+    if (i >= m.count[t]) return;
+    float *w = m.w[t], *v = m.v[t], *grad = m.grad[t];
+    const float wi = w[i];
+    const float gi = grad[i] + wd * wi;
+    const float vi = alpha * v[i] + (1.f - alpha) * gi * gi;
+    const float wn = wi - lr * gi / (sqrtf(vi) + eps);
+    v[i] = vi;
+    w[i] = wn;
+    grad[i] = 0.f;
+    if (m.w16[t]) m.w16[t][i] = (uint16_t)f32_to_h16<BF16>(wn);
+}
+
 // ---------------------------------------------------------------- workspace
 
 std::mutex g_tw_mu;
@@ -473,6 +497,17 @@ hipError_t launch_conv_weight_grad(const uint16_t *x, const uint16_t *g, float *
     const unsigned grid = (unsigned)((fwd.cout / 64) * ((fwd.cin + 63) / 64) * G.k * G.k * G.splits);
     if (bf16) hipLaunchKernelGGL(k_wgrad16<true>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, db, G);
     else hipLaunchKernelGGL(k_wgrad16<false>, dim3(grid), dim3(kThreads), 0, s, x, g, dw, db, G);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsprop_many(const RmspropMany &m, float lr, float alpha, float eps, float wd,
+                               bool bf16, hipStream_t s)
+{
+    const dim3 grid((unsigned)m.first[m.n]), block(kThreads);
+    if (bf16)
+        hipLaunchKernelGGL(k_rmsprop_many<true>, grid, block, 0, s, m, lr, alpha, eps, wd);
+    else
+        hipLaunchKernelGGL(k_rmsprop_many<false>, grid, block, 0, s, m, lr, alpha, eps, wd);
     return hipGetLastError();
 }
 

@@ -258,11 +258,11 @@ class PolicyNet:
     def update(self, lr=1e-4, alpha=0.99, eps=1e-8, weight_decay=1e-3, stream=None):
         """One RMSprop step on every weight and bias with the accumulated gradients (which
         it resets); the 16-bit weights the convolutions read are rewritten."""
+        params = []
         for i in range(len(self.layers)):
-            bc.bc_rmsprop_step(self.master[i], self.v_w[i], self.dw[i], lr, alpha, eps, weight_decay,
-                               self.weights[i], stream)
-            bc.bc_rmsprop_step(self.biases[i], self.v_b[i], self.db[i], lr, alpha, eps, weight_decay,
-                               None, stream)
+            params.append((self.master[i], self.v_w[i], self.dw[i], self.weights[i]))
+            params.append((self.biases[i], self.v_b[i], self.db[i], None))
+        bc.bc_rmsprop_step_many(params, lr, alpha, eps, weight_decay, stream)
 
     def train_step(self, reward, mask, prob, stream=None, **rmsprop):
         """The online update of Section 4: backward pass at the last forward pass, then one

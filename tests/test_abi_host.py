@@ -31,7 +31,7 @@ def test_header_declares_the_boundary():
               "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
               "bc_block_rewards", "bc_sparse_upsample_add", "bc_policy_input", "bc_policy_probabilities",
               "bc_policy_logit_grad", "bc_grad_combine", "bc_conv2d_input_grad", "bc_conv2d_weight_grad",
-              "bc_rmsprop_step"]:
+              "bc_rmsprop_step", "bc_rmsprop_step_many"]:
         assert n in names
 
 
@@ -275,6 +275,19 @@ def test_training_validation_codes(B):
     assert rp(n=0) == B.BC_ERR_SHAPE and rp(n=(1 << 31) + 1) == B.BC_ERR_SHAPE
     assert rp(w16=FAKE_OUT, dt=0) == B.BC_ERR_DTYPE
     assert rp(v=FAKE_IN + 400) == B.BC_ERR_ALIAS and rp(w16=FAKE_RES + 8) == B.BC_ERR_ALIAS
+    # several tensors in one launch
+    P2 = B.bc_param * 2
+    two = lambda a, b: P2(B.bc_param(*a), B.bc_param(*b))
+    ok1 = (FAKE_IN, FAKE_W, FAKE_RES, None, 1000)
+    ok2 = (FAKE_IN + 8192, FAKE_W + 8192, FAKE_RES + 8192, FAKE_OUT, 500)
+    rm = lambda ps, n=2, dt=1: lib.bc_rmsprop_step_many(ps, n, f(1e-4), f(0.99), f(1e-8), f(1e-3), dt, None)
+    assert rm(None) == B.BC_ERR_NULL
+    assert rm(two(ok1, ok2), n=0) == B.BC_ERR_SHAPE and rm(two(ok1, ok2), n=65) == B.BC_ERR_SHAPE
+    assert rm(two(ok1, (FAKE_IN + 8192, FAKE_W + 8192, None, None, 500))) == B.BC_ERR_NULL
+    assert rm(two(ok1, (FAKE_IN + 8192, FAKE_W + 8192, FAKE_RES + 8192, None, 0))) == B.BC_ERR_SHAPE
+    assert rm(two(ok1, ok2), dt=0) == B.BC_ERR_DTYPE
+    assert rm(two(ok1, (FAKE_IN + 2000, FAKE_W + 8192, FAKE_RES + 8192, None, 500))) == B.BC_ERR_ALIAS
+    assert rm(two(ok1, (FAKE_IN + 8192, FAKE_W + 8192, FAKE_RES + 8192, FAKE_RES + 100, 500))) == B.BC_ERR_ALIAS
     assert B.bc_last_error()
 
 

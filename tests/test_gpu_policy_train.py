@@ -89,6 +89,28 @@ def test_rmsprop_step_matches_oracle(R):
     assert max_abs_rel(w16.float().cpu().numpy(), want_w) <= 2 ** -8
 
 
+def test_rmsprop_step_many_matches_oracle(R):
+    """Three tensors of different sizes in one launch (a ragged last workgroup each), the
+    middle one without a 16-bit copy; each element against the oracle's step."""
+    bc, _ = R
+    r = synth.rng(511)
+    sizes = [5000, 64, 1]
+    host = [tuple(a.astype(np.float32) for a in (r.normal(0, 1, n), r.uniform(0, 1e-2, n), r.normal(0, 1, n)))
+            for n in sizes]
+    dev = [tuple(torch.from_numpy(a.copy()).cuda() for a in h) for h in host]
+    w16 = [torch.zeros(n, dtype=torch.bfloat16, device="cuda") for n in sizes]
+    bc.bc_rmsprop_step_many([(w, v, g, None if i == 1 else w16[i]) for i, (w, v, g) in enumerate(dev)],
+                            1e-4, 0.99, 1e-8, 1e-3)
+    for i, ((w0, v0, g0), (w, v, g)) in enumerate(zip(host, dev)):
+        want_w, want_v = P.rmsprop_step(w0, v0, g0)
+        assert max_abs_rel(w.cpu().numpy(), want_w) <= 1e-6
+        assert max_abs_rel(v.cpu().numpy(), want_v) <= 1e-5
+        assert (g.cpu().numpy() == 0).all()
+        if i != 1:
+            assert max_abs_rel(w16[i].float().cpu().numpy(), want_w) <= 2 ** -8
+    assert (w16[1].float().cpu().numpy() == 0).all()      # no copy requested: untouched
+
+
 def test_train_step_changes_the_policy(R):
     """An update moves the weights the forward pass reads (same probabilities before the
     step, different after)."""
