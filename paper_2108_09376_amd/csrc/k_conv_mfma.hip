@@ -1165,10 +1165,12 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 // ResNet-50 frames, 0.6446 -> 0.6330 ms at 30 % active, 0.4699 -> 0.4602 at 10 %);
 // splitting K in two pays off when a full frame has at most 256 tiles (the stride-32
 // layers) and for 3x3 layers with 512 or more input channels and 513 to 2048 tiles
-// (where nine-tap stages do not apply); stride-32 1x1 layers with 16 or more chunks
-// split K in three (0.6410 -> 0.6384 ms at 30 %, no cost at 50 or 100 %; three slices
-// of the nine-tap 3x3 layers gain at 10-30 % but lose 2 % at 50-100 %, where their
-// workgroups outnumber the CUs).
+// (where nine-tap stages do not apply); 1x1 layers with at most 256 tiles split K in
+// three from 32 chunks on (ResNet-50's stride-32 2048->512: 0.6410 -> 0.6384 ms at 30 %,
+// no cost at 50 or 100 %) and not below (SwiftNet's decoder laterals with 8 and 16
+// chunks: 7.3 -> 5.3 and 7.2 -> 6.6 us unsplit); three slices of the nine-tap 3x3
+// layers gain at 10-30 % but lose 2 % at 50-100 %, where their workgroups outnumber
+// the CUs.
 // Other forms take the largest tile with >= 2048 workgroups on a full frame. The choice
 // depends on the layer's shape only, never on the active count, so an active block's
 // result does not depend on which other blocks are active.
@@ -1182,14 +1184,14 @@ bool choose_plan(const LayerGeom &g, Plan &best)
             MfmaArgs &a = best.a;
             const int nchunk = (g.cin + BK - 1) / BK;
             const unsigned tiles = best.grid;
-            // split K in two for few tiles with a long K (three for 1x1 layers with 16 or
-            // more chunks), and for 3x3 layers with at least 512 input channels (sixteen
-            // chunks of nine taps per tile otherwise) whose tiles are too many for nine-tap
-            // stages
-            const bool split = (tiles <= 256 && nchunk >= 8) ||
+            // split K for few tiles with a long K (3x3: two slices from 8 chunks; 1x1:
+            // three slices from 32 chunks, shorter 1x1 slices do not pay for the hand-off),
+            // and in two for 3x3 layers with at least 512 input channels (sixteen chunks of
+            // nine taps per tile otherwise) whose tiles are too many for nine-tap stages
+            const bool split = (tiles <= 256 && nchunk >= (g.kh == 1 ? 32 : 8)) ||
                                (g.kh == 3 && nchunk >= 16 && tiles > 512 && tiles <= 2048);
             if (best.BM == 64 && best.BN == 64 && split && tiles <= (unsigned)kMaxSplitTiles) {
-                const int ns = (g.kh == 1 && tiles <= 256 && nchunk >= 16) ? 3 : 2;
+                const int ns = g.kh == 1 ? 3 : 2;
                 a.cps = (nchunk + ns - 1) / ns;
                 a.ksplit = (nchunk + a.cps - 1) / a.cps;
                 best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);

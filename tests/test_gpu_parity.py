@@ -168,6 +168,8 @@ CASES = [
                                                         # resident workgroups: several each
     (3, 64, 64, 63, 2, 4, 7, 2, True, False, 0.5),      # stem form, odd input width: pixels
                                                         # staged one channel at a time
+    (1024, 64, 16, 32, 2, 4, 1, 1, True, True, 0.5),    # 1x1, 32 chunks on a few tiles: K split
+                                                        # in three (11, 11, 10 chunks)
 ]
 
 
