@@ -261,7 +261,7 @@ __device__ __forceinline__ IgPart ig_part(const IgGeom &g)
 // Workgroup maximum (butterfly within each wave, then across the waves) into the
 // block's slot by an integer atomic max: the values are >= 0, whose IEEE bit patterns
 // order like the numbers, and the slot starts at +0.
-__device__ __forceinline__ void block_max_out(float best, float *wave_max, float *slot)
+__device__ __forceinline__ void block_max_out(float best, float *wave_max, float *slot, bool whole)
 {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) best = fmaxf(best, __shfl_xor(best, o));
@@ -271,7 +271,12 @@ __device__ __forceinline__ void block_max_out(float best, float *wave_max, float
         float m = wave_max[0];
 #pragma unroll
         for (int i = 1; i < kIgThreads / 64; ++i) m = fmaxf(m, wave_max[i]);
-        atomicMax((unsigned int *)slot, __float_as_uint(m));
+        // one workgroup per block: the value itself; else the maximum over the block's
+        // workgroups (non-negative floats order like their bit patterns)
+        if (whole)
+            *slot = m;
+        else
+            atomicMax((unsigned int *)slot, __float_as_uint(m));
     }
 }
 
@@ -304,12 +309,14 @@ __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
         const float kl = pixel_kl<CMAX>(a, b, g.classes);
         best = kl > best ? kl : best;
     }
-    block_max_out(best, wave_max, &ig[q.blk]);
+    block_max_out(best, wave_max, &ig[q.blk], g.strips == 1);
 }
 
 // Channels last, bf16/fp16 (c % 8 == 0): per pixel the CV 16-byte vectors that hold the
-// class scores (8 channels each, CV = ceil(classes / 8)) of both maps are requested at
-// once; arithmetic in fp32 as above.
+// class scores (8 channels each, CV = ceil(classes / 8)) of both maps; a thread requests
+// those of kIgUnroll pixels before using any (pixels past the range read zeros and are
+// left out); arithmetic in fp32 as above.
+constexpr int kIgUnroll = 4;
 template <bool BF16, int CV>
 __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax_nhwc16(
     const uint4 *__restrict__ lt, const uint4 *__restrict__ lp, IgGeom g, float *__restrict__ ig)
@@ -323,29 +330,38 @@ __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax_nhwc16(
     const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(lp + q.img * img_vec), (short)0, g.bytes, kBufferFlags);
     float best = 0.f;
-    for (int p = threadIdx.x; p < q.npix; p += kIgThreads) {
-        const int y = q.y0 + p / q.bw, x = q.gx * q.bw + p % q.bw;
-        const int base = (y * g.w + x) * vpp * 16;
-        i32x4 va[CV], vb[CV];
+    for (int p0 = threadIdx.x; p0 < q.npix; p0 += kIgThreads * kIgUnroll) {
+        i32x4 va[kIgUnroll][CV], vb[kIgUnroll][CV];
 #pragma unroll
-        for (int j = 0; j < CV; ++j) {
-            va[j] = __builtin_amdgcn_raw_buffer_load_b128(rt, base + 16 * j, 0, 0);
-            vb[j] = __builtin_amdgcn_raw_buffer_load_b128(rp, base + 16 * j, 0, 0);
-        }
-        float a[8 * CV], b[8 * CV];
+        for (int u = 0; u < kIgUnroll; ++u) {
+            const int p = p0 + u * kIgThreads;
+            const int y = q.y0 + p / q.bw, x = q.gx * q.bw + p % q.bw;
+            int base = p < q.npix ? (y * g.w + x) * vpp * 16 : kOutOfRange;
+            asm volatile("" : "+v"(base));
 #pragma unroll
-        for (int j = 0; j < CV; ++j) {
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                const int sh = 16 * (t & 1);
-                a[8 * j + t] = h16_to_f32<BF16>(((uint32_t)va[j][t >> 1] >> sh) & 0xFFFFu);
-                b[8 * j + t] = h16_to_f32<BF16>(((uint32_t)vb[j][t >> 1] >> sh) & 0xFFFFu);
+            for (int j = 0; j < CV; ++j) {
+                va[u][j] = __builtin_amdgcn_raw_buffer_load_b128(rt, base + 16 * j, 0, 0);
+                vb[u][j] = __builtin_amdgcn_raw_buffer_load_b128(rp, base + 16 * j, 0, 0);
             }
         }
-        const float kl = pixel_kl<8 * CV>(a, b, g.classes);
-        best = kl > best ? kl : best;
+#pragma unroll
+        for (int u = 0; u < kIgUnroll; ++u) {
+            if (p0 + u * kIgThreads >= q.npix) break;
+            float a[8 * CV], b[8 * CV];
+#pragma unroll
+            for (int j = 0; j < CV; ++j) {
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    const int sh = 16 * (t & 1);
+                    a[8 * j + t] = h16_to_f32<BF16>(((uint32_t)va[u][j][t >> 1] >> sh) & 0xFFFFu);
+                    b[8 * j + t] = h16_to_f32<BF16>(((uint32_t)vb[u][j][t >> 1] >> sh) & 0xFFFFu);
+                }
+            }
+            const float kl = pixel_kl<8 * CV>(a, b, g.classes);
+            best = kl > best ? kl : best;
+        }
     }
-    block_max_out(best, wave_max, &ig[q.blk]);
+    block_max_out(best, wave_max, &ig[q.blk], g.strips == 1);
 }
 
 // ---------------------------------------------------------------- rewards
@@ -478,16 +494,23 @@ hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, in
                                        int gw, float *ig, hipStream_t s)
 {
     const int blocks = n * gh * gw;
-    hipLaunchKernelGGL(k_fill_zero, dim3((blocks + 255) / 256), dim3(256), 0, s, ig, blocks);
     IgGeom g;
     g.classes = classes; g.c = c; g.h = h; g.w = w; g.gh = gh; g.gw = gw;
     const int bh = h / gh, bw = w / gw;
-    // about kIgPixPerWG pixels per workgroup, a quarter of that below 2M pixels (a
-    // quarter-resolution score map) so that the launch still has >= 512 workgroups
-    const int per_wg = (long long)n * h * w >= (1LL << 21) ? kIgPixPerWG : kIgPixPerWG / 4;
-    g.rows = per_wg / bw;
-    g.rows = g.rows < 1 ? 1 : (g.rows > bh ? bh : g.rows);
+    if (nhwc && bh * bw <= 4 * kIgPixPerWG) {
+        // one workgroup per block (at most 16 pixels per thread, requested 4 at a time):
+        // its maximum is stored, no zero fill and no atomics
+        g.rows = bh;
+    } else {
+        // about kIgPixPerWG pixels per workgroup, a quarter of that below 2M pixels (a
+        // quarter-resolution score map) so that the launch still has >= 512 workgroups
+        const int per_wg = (long long)n * h * w >= (1LL << 21) ? kIgPixPerWG : kIgPixPerWG / 4;
+        g.rows = per_wg / bw;
+        g.rows = g.rows < 1 ? 1 : (g.rows > bh ? bh : g.rows);
+    }
     g.strips = (bh + g.rows - 1) / g.rows;
+    if (g.strips > 1)
+        hipLaunchKernelGGL(k_fill_zero, dim3((blocks + 255) / 256), dim3(256), 0, s, ig, blocks);
     g.bytes = (int)((size_t)c * h * w * esize);   // one image's scores (checked < 2 GiB)
     const dim3 grid((unsigned)blocks * g.strips), block(kIgThreads);
     const float *a = (const float *)lt, *b = (const float *)lp;

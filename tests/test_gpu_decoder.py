@@ -128,6 +128,8 @@ def _ig_nhwc(B, lt_bits, lp_bits, dtype, classes, grid):
     ("bf16", 1, 32, 32, 16, 48, (2, 3)),
     ("f16", 1, 9, 16, 24, 24, (3, 3)),
     ("bf16", 1, 1, 8, 16, 16, (2, 2)),          # one class: KL is 0
+    ("bf16", 1, 19, 24, 256, 256, (4, 4)),      # 4096-pixel blocks: one workgroup, 16 pixels a thread
+    ("bf16", 1, 19, 24, 256, 256, (2, 2)),      # 16384-pixel blocks: several workgroups per block
 ])
 def test_information_gain_nhwc_parity(B, dtype, n, classes, c, h, w, grid):
     r = synth.rng(330 + c + classes)
