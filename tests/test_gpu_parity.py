@@ -170,6 +170,8 @@ CASES = [
                                                         # staged one channel at a time
     (1024, 64, 16, 32, 2, 4, 1, 1, True, True, 0.5),    # 1x1, 32 chunks on a few tiles: K split
                                                         # in three (11, 11, 10 chunks)
+    (256, 128, 64, 128, 8, 16, 3, 1, True, True, 0.3),  # 3x3, 8 chunks on 256 tiles: K split in
+                                                        # two, nine-tap stages
 ]
 
 
@@ -259,7 +261,7 @@ def test_conv_mfma_batch(B, case):
     assert max_abs_rel(oracle.value(got[sel], "bf16"), oracle.value(want[sel], "bf16")) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("case", [CASES[1], CASES[2], CASES[5], CASES[7]])
+@pytest.mark.parametrize("case", [CASES[1], CASES[2], CASES[5], CASES[7], CASES[-1]])
 def test_conv_active_bits_independent_of_mask(B, case):
     """An active block's bits do not depend on which other blocks are active."""
     got_sparse, _, mask, _ = _conv_case(B, "bf16", case, seed=93)
