@@ -2,6 +2,7 @@
 // error text, the persistent-buffer registry and kernel dispatch. Every check runs
 // before anything is enqueued; kernels are launched on the caller's stream.
 #include <math.h>
+#include <algorithm>
 #include <cmath>
 #include <vector>
 #include <stdarg.h>
@@ -867,10 +868,12 @@ bc_status bc_rmsprop_step_many(const bc_param *params, int32_t n, float lr, floa
         spans.push_back({params[t].grad, b});
         if (params[t].w16) spans.push_back({params[t].w16, (size_t)params[t].count * 2});
     }
-    for (size_t i = 0; i < spans.size(); ++i)
-        for (size_t j = i + 1; j < spans.size(); ++j)
-            if (overlap(spans[i].p, spans[i].b, spans[j].p, spans[j].b))
-                return fail(BC_ERR_ALIAS, "the optimiser's buffers overlap");
+    // sorted by start address, any overlap shows between neighbours
+    std::sort(spans.begin(), spans.end(),
+              [](const Span &x, const Span &y) { return (uintptr_t)x.p < (uintptr_t)y.p; });
+    for (size_t i = 0; i + 1 < spans.size(); ++i)
+        if (overlap(spans[i].p, spans[i].b, spans[i + 1].p, spans[i + 1].b))
+            return fail(BC_ERR_ALIAS, "the optimiser's buffers overlap");
     hipError_t e = bc::launch_rmsprop_many(m, lr, alpha, eps, weight_decay, dtype == BC_BF16,
                                            (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "rmsprop launch");
