@@ -403,10 +403,11 @@ def swiftnet_clip_step(torch, bc, dev, frames=30, seed=2021):
       1. execution grid sampled from the policy's block probabilities, index built
          (bc_sample_execution_grid);
       2. frame state: executed blocks of the RGB frame copied (bc_update_frame_state);
-      3. the previous class scores saved (a full-buffer bc_update_frame_state);
+      3. the previous class scores of the blocks about to run saved
+         (bc_update_frame_state with the index);
       4. the sparse network on the sampled index (42 layers incl. 3 upsample merges);
       5. information gain of the stride-4 scores (19 of 64 channels) against the saved
-         ones (bc_seg_information_gain);
+         ones on the executed blocks, 0 elsewhere (bc_seg_information_gain with the grid);
       6. rewards, cost, moving average and REINFORCE loss (bc_block_rewards).
     The policy network is not part of the step: its stand-in output is p = 1 on the
     blocks the clip's objects touch at t or t-1 and 0.05 elsewhere (exploration),
@@ -443,14 +444,14 @@ def swiftnet_clip_step(torch, bc, dev, frames=30, seed=2021):
     def before():
         bc.bc_sample_execution_grid(prob, grid, seed, 1, mask, idx, cnt)
         bc.bc_update_frame_state(x, state, bc.BC_NHWC, grid, idx, cnt)
-        bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, grid, None, None)
+        bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, grid, idx, cnt)
 
     def network():
         net.frame(x, sparse=True, index=(idx, cnt))
 
     def after():
         bc.bc_seg_information_gain(net.logits, prev_logits, grid, ig, classes=net.classes,
-                                   layout=bc.BC_NHWC)
+                                   layout=bc.BC_NHWC, mask=mask)
         bc.bc_block_rewards(ig, mask, prob, grid, 0.3, 5.0, 0.9, mavg, reward, cost, loss)
 
     def restart():

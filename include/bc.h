@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 6
+#define BC_ABI_VERSION 7
 
 typedef enum {
     BC_OK = 0,
@@ -298,6 +298,11 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
  *   d_logits, d_prev_logits  frame t and frame t-1, same desc: F32 NCHW
  *            [n][c][h][w], or BF16/F16 NHWC [n][h][w][c] with c % 8 == 0.
  *   classes  1 .. min(c, 32).
+ *   d_mask   the frame's execution grid, uint8 [n][grid_h][grid_w] (nonzero = the block
+ *            ran), or NULL (every block). A block that did not run gets 0 without its
+ *            scores being read (they are frame t-1's own, so the gain is exactly 0): the
+ *            caller only needs frame t-1's scores of the executed blocks in
+ *            d_prev_logits (e.g. bc_update_frame_state with the index before the frame).
  *   d_ig     float32 [n][grid_h][grid_w], device (written completely).
  * Errors: BC_ERR_NULL, BC_ERR_SHAPE (classes), BC_ERR_DTYPE (NCHW not F32, NHWC F32),
  * BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE, BC_ERR_ALIAS (d_ig overlapping an input),
@@ -305,8 +310,8 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
  * BC_ERR_HIP.
  */
 bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logits,
-                                  bc_tensor desc, int32_t classes, bc_grid g, float *d_ig,
-                                  void *stream);
+                                  bc_tensor desc, int32_t classes, bc_grid g,
+                                  const uint8_t *d_mask, float *d_ig, void *stream);
 
 /*
  * Input of the policy network (Section 3.3, Eq. 2: S_t = {I_t, H_{t-1}, A_{t-1},

@@ -78,7 +78,7 @@ _sigs = {
     "bc_update_frame_state": ([_vp, _vp, bc_tensor, bc_grid, _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_upsample_add": ([_vp, bc_tensor, _vp, _vp, bc_tensor, bc_grid, _i32, _vp, _vp, _i32,
                                 _vp], _i32),
-    "bc_seg_information_gain": ([_vp, _vp, bc_tensor, _i32, bc_grid, _vp, _vp], _i32),
+    "bc_seg_information_gain": ([_vp, _vp, bc_tensor, _i32, bc_grid, _vp, _vp, _vp], _i32),
     "bc_policy_input": ([_vp, _vp, bc_tensor, _vp, bc_tensor, _i32, _vp, bc_grid, _vp, bc_tensor, _vp], _i32),
     "bc_policy_probabilities": ([_vp, bc_tensor, _vp, _vp], _i32),
     "bc_policy_logit_grad": ([_vp, _vp, _vp, _vp, bc_tensor, _vp], _i32),
@@ -98,7 +98,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 6
+ABI_VERSION = 7
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -253,16 +253,17 @@ def bc_update_frame_state(frame, state, layout, grid, idx, count, stream=None):
 
 
 def bc_seg_information_gain(logits, prev_logits, grid, ig, classes=None, layout=BC_NCHW,
-                            stream=None):
+                            mask=None, stream=None):
     """Score maps of frames t and t-1 (float32 [n, c, h, w], or bf16/f16 [n, h, w, c] with
     layout=BC_NHWC) -> ig float32 [n, gh, gw]; the first `classes` channels (default all)
-    are the class scores."""
+    are the class scores. With the execution grid `mask` (uint8 [n, gh, gw]) blocks that
+    did not run get 0 without their scores being read."""
     if logits.shape != prev_logits.shape or logits.dtype != prev_logits.dtype:
         raise ValueError("score maps must have the same shape and dtype")
     d = desc(logits, layout)
     st = _lib.bc_seg_information_gain(_ptr(logits), _ptr(prev_logits), d,
                                       int(d.c if classes is None else classes), _grid(grid),
-                                      _ptr(ig), _stream(stream))
+                                      _ptr(mask), _ptr(ig), _stream(stream))
     _check(st, "bc_seg_information_gain")
 
 

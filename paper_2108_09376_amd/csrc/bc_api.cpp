@@ -557,8 +557,8 @@ bc_status bc_update_frame_state(const void *d_frame, void *d_state, bc_tensor de
 }
 
 bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logits,
-                                  bc_tensor desc, int32_t classes, bc_grid g, float *d_ig,
-                                  void *stream)
+                                  bc_tensor desc, int32_t classes, bc_grid g,
+                                  const uint8_t *d_mask, float *d_ig, void *stream)
 {
     if (!d_logits || !d_prev_logits || !d_ig)
         return fail(BC_ERR_NULL, "d_logits, d_prev_logits and d_ig are required");
@@ -579,11 +579,12 @@ bc_status bc_seg_information_gain(const void *d_logits, const void *d_prev_logit
     const double img_bytes = (double)es * desc.c * desc.h * desc.w;
     if (img_bytes >= 2147483392.0) return fail(BC_ERR_UNSUPPORTED, "one image's scores must be < 2 GiB");
     const size_t bytes = tensor_bytes(desc), igb = (size_t)L.total_blocks * 4;
-    if (overlap(d_ig, igb, d_logits, bytes) || overlap(d_ig, igb, d_prev_logits, bytes))
+    if (overlap(d_ig, igb, d_logits, bytes) || overlap(d_ig, igb, d_prev_logits, bytes) ||
+        overlap(d_ig, igb, d_mask, (size_t)L.total_blocks))
         return fail(BC_ERR_ALIAS, "d_ig overlaps an input");
     hipError_t e = bc::launch_seg_information_gain(
         d_logits, d_prev_logits, desc.n, desc.c, classes, desc.h, desc.w, es,
-        desc.layout == BC_NHWC, desc.dtype == BC_BF16, g.grid_h, g.grid_w, d_ig,
+        desc.layout == BC_NHWC, desc.dtype == BC_BF16, g.grid_h, g.grid_w, d_mask, d_ig,
         (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "information gain launch");
     return ok();

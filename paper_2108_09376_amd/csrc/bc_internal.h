@@ -58,7 +58,7 @@ hipError_t launch_frame_state(const void *frame, void *state, int n, int c, int 
 // `classes` of c channels, [n][c][h][w] fp32 or [n][h][w][c] bf16/fp16 (c % 8 == 0).
 hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, int c, int classes,
                                        int h, int w, int esize, bool nhwc, bool bf16, int gh,
-                                       int gw, float *ig, hipStream_t s);
+                                       int gw, const uint8_t *mask, float *ig, hipStream_t s);
 // Rewards, cost, moving average and REINFORCE loss per image.
 hipError_t launch_block_rewards(const float *ig, const uint8_t *mask, const float *prob, int n,
                                 int blocks, float tau, float gamma, float mu, float *mavg,

@@ -235,6 +235,7 @@ struct IgGeom {
     int h, w, gh, gw;
     int rows, strips;  // image rows per workgroup, workgroups per block
     int bytes;         // one image's scores in bytes (< 2 GiB)
+    const uint8_t *mask;   // execution grid [n][gh][gw] or null (every block)
 };
 
 // Which block and which rows of it a workgroup covers.
@@ -290,6 +291,10 @@ __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax(
 {
     __shared__ float wave_max[kIgThreads / 64];
     const IgPart q = ig_part(g);
+    if (g.mask && !g.mask[q.blk]) {   // not executed: its scores were copied, the gain is 0
+        if (g.strips == 1 && threadIdx.x == 0) ig[q.blk] = 0.f;
+        return;
+    }
     const size_t plane = (size_t)g.h * g.w;
     const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(lt + (size_t)q.img * g.c * plane), (short)0, g.bytes, kBufferFlags);
@@ -323,6 +328,10 @@ __global__ __launch_bounds__(kIgThreads) void k_seg_kl_blockmax_nhwc16(
 {
     __shared__ float wave_max[kIgThreads / 64];
     const IgPart q = ig_part(g);
+    if (g.mask && !g.mask[q.blk]) {   // not executed: its scores were copied, the gain is 0
+        if (g.strips == 1 && threadIdx.x == 0) ig[q.blk] = 0.f;
+        return;
+    }
     const int vpp = g.c / 8;
     const size_t img_vec = (size_t)g.h * g.w * vpp;
     const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
@@ -491,11 +500,12 @@ static void launch_ig_nhwc16(const void *lt, const void *lp, const IgGeom &g, di
 
 hipError_t launch_seg_information_gain(const void *lt, const void *lp, int n, int c, int classes,
                                        int h, int w, int esize, bool nhwc, bool bf16, int gh,
-                                       int gw, float *ig, hipStream_t s)
+                                       int gw, const uint8_t *mask, float *ig, hipStream_t s)
 {
     const int blocks = n * gh * gw;
     IgGeom g;
     g.classes = classes; g.c = c; g.h = h; g.w = w; g.gh = gh; g.gw = gw;
+    g.mask = mask;
     const int bh = h / gh, bw = w / gw;
     if (nhwc && bh * bw <= 4 * kIgPixPerWG) {
         // one workgroup per block (at most 16 pixels per thread, requested 4 at a time):

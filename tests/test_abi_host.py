@@ -165,7 +165,7 @@ def test_policy_step_validation_codes(B):
     assert lib.bc_update_frame_state(FAKE_IN, FAKE_OUT, B.bc_tensor(1, 3, 1024, 2048, 7, 1), g, FAKE_IDX, FAKE_CNT, 128, None) == B.BC_ERR_DTYPE
     # information gain: fp32 channels first or 16-bit channels last; `classes` leading channels
     sc = B.bc_tensor(1, 19, 1024, 2048, 0, 0)
-    ig = lambda d, cls=19, gg=g, out=FAKE_OUT, a=FAKE_IN, b=FAKE_W: lib.bc_seg_information_gain(a, b, d, cls, gg, out, None)
+    ig = lambda d, cls=19, gg=g, out=FAKE_OUT, a=FAKE_IN, b=FAKE_W, m=None: lib.bc_seg_information_gain(a, b, d, cls, gg, m, out, None)
     assert ig(sc, b=None) == B.BC_ERR_NULL
     assert ig(B.bc_tensor(1, 19, 1024, 2048, 1, 0)) == B.BC_ERR_DTYPE        # bf16 channels first
     assert ig(B.bc_tensor(1, 24, 256, 512, 0, 1), 19) == B.BC_ERR_DTYPE      # f32 channels last
@@ -175,6 +175,7 @@ def test_policy_step_validation_codes(B):
     assert ig(sc, 0) == B.BC_ERR_SHAPE and ig(sc, 20) == B.BC_ERR_SHAPE
     assert ig(sc, gg=B.bc_grid(3, 16)) == B.BC_ERR_NOT_DIVISIBLE
     assert ig(sc, out=FAKE_W + 64) == B.BC_ERR_ALIAS
+    assert ig(sc, m=FAKE_OUT + 100) == B.BC_ERR_ALIAS                # the grid inside d_ig
     # decoder merge: out = up2(coarse) (+ skip) on active blocks
     cs, os_ = B.bc_tensor(1, 128, 128, 256, 1, 1), B.bc_tensor(1, 128, 256, 512, 1, 1)
     up = lambda c=cs, o=os_, coarse=FAKE_IN, skip=FAKE_RES, out=FAKE_OUT, gg=g, relu=0, idx=FAKE_IDX, cnt=FAKE_CNT, cap=128: \

@@ -142,6 +142,39 @@ def test_information_gain_nhwc_parity(B, dtype, n, classes, c, h, w, grid):
     assert max_abs_rel(got, want) <= 1e-4
 
 
+@pytest.mark.parametrize("layout,grid", [("nchw_f32", (2, 4)), ("nhwc_bf16", (4, 8))])
+def test_information_gain_with_execution_grid(B, layout, grid):
+    """With the execution grid, blocks that did not run get 0 without their scores being
+    read (the previous map holds NaN there), executed blocks their gain: fp32 channels
+    first with several workgroups per block (a zero fill first) and bf16 channels last
+    (19 classes in 24 channels) with one workgroup per block."""
+    r = synth.rng(345)
+    n, classes, h, w = 2, 19, 256, 512
+    dtype = "f32" if layout == "nchw_f32" else "bf16"
+    lt = synth.to_storage_bits(synth.seg_logits(r, n, classes, h, w, cell=8), dtype)
+    lp = synth.to_storage_bits(synth.seg_logits_next(r, synth.storage_to_f64(lt, dtype).astype(np.float32),
+                                                     0.3), dtype)
+    mask = np.concatenate([synth.frac_mask(346, *grid, 0.5), synth.frac_mask(347, *grid, 0.25)])
+    want = P.seg_information_gain(synth.storage_to_f64(lt, dtype), synth.storage_to_f64(lp, dtype), *grid)
+    want = np.where(mask != 0, want, 0.0)
+    nan = synth.to_storage_bits(np.full((1,), np.nan, np.float32), dtype)[0]
+    stale = lp.copy()
+    sel = np.broadcast_to(oracle.expand_mask(mask, h // grid[0], w // grid[1]), stale.shape)
+    stale[~sel] = nan
+    ig = torch.full((n,) + grid, -1.0, device="cuda")
+    m = torch.from_numpy(mask).cuda()
+    if layout == "nchw_f32":
+        a, b = (torch.from_numpy(np.ascontiguousarray(x).view(np.float32)).cuda() for x in (lt, stale))
+        B.bc_seg_information_gain(a, b, grid, ig, mask=m)
+    else:
+        pad = lambda x: np.concatenate([x, synth.nan_canaries(r, (n, 24 - classes, h, w), dtype)], axis=1)
+        B.bc_seg_information_gain(to_dev(pad(lt), dtype), to_dev(pad(stale), dtype), grid, ig,
+                                  classes=classes, layout=B.BC_NHWC, mask=m)
+    got = ig.cpu().numpy().astype(np.float64)
+    assert (got[mask == 0] == 0.0).all()
+    assert max_abs_rel(got[mask != 0], want[mask != 0]) <= 1e-4
+
+
 def test_information_gain_nhwc_full_size(B):
     """19 classes in 64 channels at a quarter of 2048x1024 (512x256), 8x16 grid."""
     r = synth.rng(340)

@@ -150,14 +150,17 @@ def test_runner_refuses_sparse_frame_before_full_frame(R):
     torch.cuda.synchronize()
 
 
-def test_blockcopy_step_on_swiftnet(R):
+@pytest.mark.parametrize("sparse_save", [False, True])
+def test_blockcopy_step_on_swiftnet(R, sparse_save):
     """One BlockCopy step after a full first frame, all on the device: execution grid
     sampled from the policy's probabilities (bit for bit against the oracle's
     sampling), frame state updated (bit for bit), the segmentation network run on the
     sampled index, information gain of the new class scores against the saved previous
     ones, rewards. Checked against oracle-only values: blocks that did not run copied
     their scores, so their gain is exactly 0 and their reward -gamma (tau - M_t); the
-    cost and moving average follow from the oracle's grid."""
+    cost and moving average follow from the oracle's grid. sparse_save: only the blocks
+    about to run are saved and the gain takes the grid; its values must equal those of
+    the full save bit for bit."""
     bc, resnet = R
     h, w, tau, gamma, mu, seed, t = 256, 512, 0.3, 5.0, 0.9, 77, 1
     net = resnet.SparseSwiftNet(18, h, w, 128)
@@ -181,9 +184,18 @@ def test_blockcopy_step_on_swiftnet(R):
     # the step
     bc.bc_sample_execution_grid(p, net.grid, seed, t, mask, idx, cnt)
     bc.bc_update_frame_state(x1, state, bc.BC_NHWC, net.grid, idx, cnt)
-    bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, net.grid, None, None)
+    full_prev = torch.empty_like(net.logits)
+    bc.bc_update_frame_state(net.logits, full_prev, bc.BC_NHWC, net.grid, None, None)
+    if sparse_save:
+        prev_logits.fill_(float("nan"))               # stale everywhere the step does not save
+        bc.bc_update_frame_state(net.logits, prev_logits, bc.BC_NHWC, net.grid, idx, cnt)
+    else:
+        prev_logits.copy_(full_prev)
     net.frame(x1, sparse=True, index=(idx, cnt))
-    bc.bc_seg_information_gain(net.logits, prev_logits, net.grid, ig, classes=net.classes, layout=bc.BC_NHWC)
+    bc.bc_seg_information_gain(net.logits, prev_logits, net.grid, ig, classes=net.classes, layout=bc.BC_NHWC,
+                               mask=mask if sparse_save else None)
+    ig_full = torch.empty_like(ig)
+    bc.bc_seg_information_gain(net.logits, full_prev, net.grid, ig_full, classes=net.classes, layout=bc.BC_NHWC)
     bc.bc_block_rewards(ig, mask, p, net.grid, tau, gamma, mu, mavg, reward, cost, loss)
     torch.cuda.synchronize()
     m = mask.cpu().numpy()
@@ -192,6 +204,7 @@ def test_blockcopy_step_on_swiftnet(R):
     assert np.array_equal(from_dev(state), P.update_frame_state(b1, b0, want_mask, "nchw"))
     g = ig.cpu().numpy()
     assert (g[want_mask == 0] == 0.0).all() and (g[want_mask == 1] > 0.0).all()
+    assert np.array_equal(g, ig_full.cpu().numpy())
     _, want_c, want_m = P.block_rewards(np.zeros_like(g, np.float64), want_mask, tau, gamma, mu, [0.5])
     assert abs(float(cost.item()) - want_c[0]) <= 1e-6 and abs(float(mavg.item()) - want_m[0]) <= 1e-6
     rw = reward.cpu().numpy().astype(np.float64)
