@@ -262,7 +262,8 @@ def policy_steps(torch, bc, dev):
       block_rewards     rewards, cost, moving average and loss over 128 blocks
       seg_information_gain_nhwc  the segmentation network's own output: bf16 scores at
                         stride 4 (512x256), 19 classes in 64 channels; algorithmic bytes
-                        = the 19 class scores of both maps once
+                        = the 19 class scores of both maps once; line bytes = the
+                        128-byte lines that hold them (all 64 channels), fetched whole
       upsample_add      the decoder's largest merge (128x256 -> 256x512, 128 channels,
                         bf16, skip added, 38 blocks); algorithmic bytes = the active
                         blocks' coarse tiles with their one-pixel halo and skip read
@@ -340,6 +341,12 @@ def policy_steps(torch, bc, dev):
         if nbytes:
             row.update({"bytes": nbytes, "GBps": round(nbytes / us / 1e3, 1),
                         "frac_of_hbm_peak": round(nbytes / us / 1e3 / PEAK_HBM_GBS, 3)})
+        if name == "seg_information_gain_nhwc":
+            # every pixel's 19 class scores lie in one 128-byte line of its 64 channels:
+            # both maps' lines are fetched whole
+            lines = 2 * 256 * 512 * 128
+            row.update({"line_bytes": lines, "line_GBps": round(lines / us / 1e3, 1),
+                        "line_frac_of_hbm_peak": round(lines / us / 1e3 / PEAK_HBM_GBS, 3)})
         if name == "policy_forward":
             row.update({"gmac": round(pnet.macs() / 1e9, 3),
                         "tflops": round(2 * pnet.macs() / us / 1e6, 1)})
