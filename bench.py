@@ -632,7 +632,7 @@ def main():
         print(pmc_summary(*args.pmc_summary))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
     import numpy as np
     import torch

@@ -19,8 +19,8 @@ where conv is the ordinary dense layer on the layer's current input buffer X_t
 (fresh where the neighbour block was executed this frame, transferred otherwise),
 and select keeps Y_{t-1} bit for bit outside the selected blocks. The oracle takes
 exactly these steps: a dense convolution everywhere (C, fp64, ``bc_oracle.c``),
-rounding to the storage format, then the masked select. Readings of points the
-paper leaves open are listed in the design doc's readings table; the ones used here:
+rounding to the storage format, then the masked select. Points the paper leaves
+open are read as follows:
 
 * the mask indexes *output* blocks; block (gy, gx) of a layer with output block
   edge bh x bw covers output rows gy*bh .. gy*bh+bh-1 (same for columns);
