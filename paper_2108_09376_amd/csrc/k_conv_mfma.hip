@@ -1200,9 +1200,12 @@ bool choose_plan(const LayerGeom &g, Plan &best)
             // Stage grouping (3x3): with at most 512 tiles on a full frame (the stride-16
             // and stride-32 layers: few workgroups, long K) staging all nine taps of a
             // chunk under one barrier is faster; with more tiles the smaller LDS footprint
-            // of one tap per barrier keeps more workgroups resident, which wins. SG does
-            // not change the summation order.
-            if (g.kh == 3 && best.BM == 64 && best.BN == 64 && best.tiles <= 512 && a.cps >= 2) {
+            // of one tap per barrier keeps more workgroups resident, which wins. A call
+            // without an index runs every tile: there nine-tap stages (one workgroup per
+            // CU) need the tiles to fit one round, at most 256. SG does not change the
+            // summation order, so this choice never changes a result.
+            const unsigned sg9_tiles = g.count ? 512u : 256u;
+            if (g.kh == 3 && best.BM == 64 && best.BN == 64 && best.tiles <= sg9_tiles && a.cps >= 2) {
                 const size_t lds = pipe_lds(a.nslot, best.BM, best.BN, 9, 9);
                 if (lds <= kMaxLdsPipe) {
                     best.sg = 9;
