@@ -1184,14 +1184,15 @@ bool choose_plan(const LayerGeom &g, Plan &best)
             MfmaArgs &a = best.a;
             const int nchunk = (g.cin + BK - 1) / BK;
             const unsigned tiles = best.grid;
-            // split K for few tiles with a long K (3x3: two slices from 8 chunks; 1x1:
-            // three slices from 32 chunks, shorter 1x1 slices do not pay for the hand-off),
+            // split K for few tiles with a long K (3x3: two slices from 8 chunks, four
+            // with at most 64 tiles; 1x1: three slices from 32 chunks, shorter 1x1 slices
+            // do not pay for the hand-off),
             // and in two for 3x3 layers with at least 512 input channels (sixteen chunks of
             // nine taps per tile otherwise) whose tiles are too many for nine-tap stages
             const bool split = (tiles <= 256 && nchunk >= (g.kh == 1 ? 32 : 8)) ||
                                (g.kh == 3 && nchunk >= 16 && tiles > 512 && tiles <= 2048);
             if (best.BM == 64 && best.BN == 64 && split && tiles <= (unsigned)kMaxSplitTiles) {
-                const int ns = g.kh == 1 ? 3 : 2;
+                const int ns = g.kh == 1 ? 3 : (tiles <= 64 && nchunk >= 8 ? 4 : 2);
                 a.cps = (nchunk + ns - 1) / ns;
                 a.ksplit = (nchunk + a.cps - 1) / a.cps;
                 best.ws_bytes = (size_t)tiles * a.ksplit * best.BM * best.BN * sizeof(float);

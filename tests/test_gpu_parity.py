@@ -160,7 +160,7 @@ CASES = [
     (40, 64, 48, 80, 3, 5, 3, 1, True, False, 0.6),     # Cin not a multiple of 32: ragged K chunk
     (64, 192, 64, 64, 4, 4, 5, 1, True, True, 0.5),     # 5x5, Cout=192
     (128, 128, 48, 48, 12, 12, 3, 1, True, True, 0.33), # 4x4 blocks, ragged tail of patches
-    (512, 64, 32, 64, 4, 8, 3, 1, True, True, 0.5),     # 16 chunks on a few tiles: K split in 2
+    (512, 64, 32, 64, 4, 8, 3, 1, True, True, 0.5),     # 16 chunks on 32 tiles: K split in 4
     (3, 64, 32, 64, 2, 4, 1, 1, True, False, 0.5),      # 1x1 with Cin=3 (stem form)
     (5, 64, 32, 64, 2, 4, 3, 1, True, True, 0.5),       # Cin=5: 8 padded channels per pixel
     (3, 64, 64, 64, 2, 2, 7, 1, True, False, 0.5),      # 7x7/1 stem form (unaligned rows)
