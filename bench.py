@@ -150,6 +150,39 @@ def layer_sweep(torch, bc, dev):
     return out
 
 
+def measured_ceilings(torch, dev):
+    """Context for the roofline denominators (the published peaks stay the reference):
+    torch's bf16 matrix product through the vendor library on an 8192-cube (the largest
+    dense contraction rate a library reaches here), and torch's device copy of 1 GiB."""
+    a = torch.randn((8192, 8192), device=dev).to(torch.bfloat16)
+    b = torch.randn((8192, 8192), device=dev).to(torch.bfloat16)
+    c = torch.empty((8192, 8192), device=dev, dtype=torch.bfloat16)
+    src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def per_call_ms(fn, reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    gemm_ms = per_call_ms(lambda: torch.matmul(a, b, out=c), 20)
+    copy_ms = per_call_ms(lambda: dst.copy_(src), 20)
+    gemm_tf = 2 * 8192 ** 3 / (gemm_ms * 1e-3) / 1e12
+    copy_gbs = 2 * src.numel() * 2 / (copy_ms * 1e-3) / 1e9
+    del a, b, c, src, dst
+    return {"bf16_gemm_8192_TFLOPs": round(gemm_tf, 1),
+            "bf16_gemm_frac_of_peak": round(gemm_tf / PEAK_BF16_TFLOPS, 3),
+            "copy_1GiB_GBps": round(copy_gbs, 1),
+            "copy_frac_of_peak": round(copy_gbs / PEAK_HBM_GBS, 3)}
+
+
 def gather_scatter(torch, bc, dev):
     """Standalone halo gather and block scatter on the 256x512 stride-4 map of a
     2048x1024 frame (32-px blocks, 38 of 128 active, 3x3 halo), C = 64 and 256, bf16.
@@ -813,6 +846,7 @@ def main():
                      "trace_conv_dispatch_window": conv_window,
                      "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
+    out["measured_ceilings"] = measured_ceilings(torch, dev)
     if not args.no_layer_sweep:
         out["single_layers_at_0.3"] = layer_sweep(torch, bc, dev)
     if not args.no_gather_scatter:
