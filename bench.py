@@ -105,16 +105,17 @@ def cpu_baseline(mask):
 def layer_sweep(torch, bc, dev):
     """Single block-sparse layers at their 2048x1024-frame shapes, 38 of 128 blocks
     active (clustered): the stride-4 3x3 64->64 layer (256x512, 32-px blocks) and the
-    stride-16 sweep (64x128, 8-px blocks), 1x1 and 3x3 with Cin = Cout in {256, 512,
-    1024}. Each is timed as a captured graph of 10 launches; FLOPs are algorithmic
-    (2*Cin*Cout*k*k per active output pixel)."""
+    stride-16 sweep (64x128, 8-px blocks), 1x1 and 3x3 with Cin and Cout in {256, 512,
+    1024} (all nine pairs). Each is timed as a captured graph of 10 launches; FLOPs are
+    algorithmic (2*Cin*Cout*k*k per active output pixel)."""
     import numpy as np
 
     import synth
     shapes = [("3x3 64->64 @256x512", 64, 64, 256, 512, 3)]
-    for c in (256, 512, 1024):
-        for k in (1, 3):
-            shapes.append((f"{k}x{k} {c}->{c} @64x128", c, c, 64, 128, k))
+    for cin in (256, 512, 1024):
+        for cout in (256, 512, 1024):
+            for k in (1, 3):
+                shapes.append((f"{k}x{k} {cin}->{cout} @64x128", cin, cout, 64, 128, k))
     mask = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
     m = torch.from_numpy(mask).to(dev)
     idx = torch.empty(128, dtype=torch.int32, device=dev)
@@ -143,9 +144,14 @@ def layer_sweep(torch, bc, dev):
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / 50
-        fl = 2.0 * cin * cout * k * k * h * w * int(mask.sum()) / mask.size
+        n_act = int(mask.sum())
+        fl = 2.0 * cin * cout * k * k * h * w * n_act / mask.size
+        # algorithmic bytes: the active blocks' halo tiles, outputs and the weights, once
+        bh, bw = h // 8, w // 16
+        nb = n_act * ((bh + k - 1) * (bw + k - 1) * cin + bh * bw * cout) * 2 + cout * k * k * cin * 2
         out[name] = {"us": round(us, 2), "tflops": round(fl / us / 1e6, 1),
-                     "frac_of_mfma_peak": round(fl / us / 1e6 / PEAK_BF16_TFLOPS, 4)}
+                     "frac_of_mfma_peak": round(fl / us / 1e6 / PEAK_BF16_TFLOPS, 4),
+                     "bytes": nb, "frac_of_hbm_peak": round(nb / us / 1e3 / PEAK_HBM_GBS, 4)}
         del g
     return out
 
