@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch layer by layer instead of a HIP graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gather-scatter", action="store_true")
+    ap.add_argument("--no-vendor-dense", action="store_true",
+                    help="skip the dense frame through torch's own convolutions")
     ap.add_argument("--no-clip", action="store_true",
                     help="skip the 30-frame clip (ResNet-18 encoder; SwiftNet-18 full step)")
     ap.add_argument("--no-policy-steps", action="store_true",
@@ -154,6 +156,54 @@ def layer_sweep(torch, bc, dev):
                      "bytes": nb, "frac_of_hbm_peak": round(nb / us / 1e3 / PEAK_HBM_GBS, 4)}
         del g
     return out
+
+
+def vendor_dense_frame(torch, dev, layers):
+    """The same ResNet-50 frame dense through torch's own convolutions (the vendor
+    library, its default algorithm search), random weights of the same shapes, one
+    captured graph per frame: what a dense frame costs without this library."""
+    import torch.nn.functional as F
+    params = []
+    for l in layers:
+        if l.kind != "conv":
+            params.append(None)
+            continue
+        w = (torch.randn(l.cout, l.cin, l.k, l.k, device=dev) * (2.0 / (l.cin * l.k * l.k)) ** 0.5)
+        params.append((w.to(torch.bfloat16).contiguous(memory_format=torch.channels_last),
+                       torch.zeros(l.cout, device=dev, dtype=torch.bfloat16)))
+    x = torch.randn(1, 3, 1024, 2048, device=dev).to(torch.bfloat16).contiguous(memory_format=torch.channels_last)
+
+    def frame():
+        outs = []
+        for l, p in zip(layers, params):
+            src = x if l.src < 0 else outs[l.src]
+            if l.kind == "pool":
+                y = F.max_pool2d(src, l.k, l.stride, l.pad)
+            else:
+                y = F.conv2d(src, p[0], p[1], stride=l.stride, padding=l.pad)
+                if l.res is not None:
+                    y = y + outs[l.res]
+                if l.relu:
+                    y = F.relu(y)
+            outs.append(y)
+        return outs[-1]
+
+    for _ in range(3):
+        frame()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        frame()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) / 10
 
 
 def measured_ceilings(torch, dev):
@@ -853,6 +903,13 @@ def main():
                      "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
     out["measured_ceilings"] = measured_ceilings(torch, dev)
+    if not args.no_vendor_dense:
+        vms = vendor_dense_frame(torch, dev, net.layers)
+        out["vendor_dense_frame"] = {
+            "library": "torch conv2d (MIOpen), bf16 channels-last, residual and ReLU as torch ops",
+            "ms": round(vms, 4), "ours_every_block_ms": sweep.get("1"),
+            "ours_at_active_fraction_ms": round(ms, 4),
+            "speedup_of_this_frame": round(vms / ms, 2)}
     if not args.no_layer_sweep:
         out["single_layers_at_0.3"] = layer_sweep(torch, bc, dev)
     if not args.no_gather_scatter:
