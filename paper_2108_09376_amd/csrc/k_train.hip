@@ -127,14 +127,12 @@ __global__ __launch_bounds__(kThreads) void k_grad_combine16(const uint4 *__rest
 }
 
 // W [co][kh][kw][ci] -> W' [ci][kh][kw][co], taps reversed
-__global__ __launch_bounds__(kThreads) void k_flip_transpose16(const uint16_t *__restrict__ w,
-                                                               uint16_t *__restrict__ wt, int cout,
-                                                               int k, int cin)
+// W' [ci][i][j][co] = W[co][k-1-i][k-1-j][ci]: the weights of the transposed convolution
+__device__ __forceinline__ void flip_transpose_at(const uint16_t *__restrict__ w,
+                                                  uint16_t *__restrict__ wt, int cout, int k,
+                                                  int cin, int t)
 {
-    const int t = blockIdx.x * kThreads + threadIdx.x;
-    const int total = cout * k * k * cin;
-    if (t >= total) return;
-    // t indexes W' = [ci][i][j][co]
+    if (t >= cout * k * k * cin) return;
     const int co = t % cout;
     int r = t / cout;
     const int j = r % k;
@@ -145,13 +143,10 @@ __global__ __launch_bounds__(kThreads) void k_flip_transpose16(const uint16_t *_
 }
 
 // Z [n][2h][2w][C]: Z[2y][2x] = G[y][x], zero elsewhere (16-byte vectors, C % 8 == 0)
-__global__ __launch_bounds__(kThreads) void k_zero_insert16(const uint4 *__restrict__ g,
-                                                            uint4 *__restrict__ z, int n, int h,
-                                                            int w, int vpp)
+__device__ __forceinline__ void zero_insert_at(const uint4 *__restrict__ g, uint4 *__restrict__ z,
+                                               int n, int h, int w, int vpp, long long t)
 {
-    const long long t = (long long)blockIdx.x * kThreads + threadIdx.x;
-    const long long total = (long long)n * 4 * h * w * vpp;
-    if (t >= total) return;
+    if (t >= (long long)n * 4 * h * w * vpp) return;
     const int v = (int)(t % vpp);
     long long r = t / vpp;
     const int x = (int)(r % (2 * w));
@@ -161,6 +156,20 @@ __global__ __launch_bounds__(kThreads) void k_zero_insert16(const uint4 *__restr
     uint4 o = make_uint4(0u, 0u, 0u, 0u);
     if (!(x & 1) && !(y & 1)) o = g[(((long long)img * h + (y >> 1)) * w + (x >> 1)) * vpp + v];
     z[t] = o;
+}
+
+// Both inputs of the transposed convolution in one launch: workgroups below wblocks
+// flip the weights, the rest (none at stride 1) spread the output gradient.
+__global__ __launch_bounds__(kThreads) void k_input_grad_prep16(
+    const uint16_t *__restrict__ w, uint16_t *__restrict__ wt, int cout, int k, int cin,
+    unsigned wblocks, const uint4 *__restrict__ g, uint4 *__restrict__ z, int n, int h, int wd,
+    int vpp)
+{
+    if (blockIdx.x < wblocks)
+        flip_transpose_at(w, wt, cout, k, cin, (int)(blockIdx.x * kThreads + threadIdx.x));
+    else
+        zero_insert_at(g, z, n, h, wd, vpp,
+                       (long long)(blockIdx.x - wblocks) * kThreads + threadIdx.x);
 }
 
 // ---------------------------------------------------------------- weight gradient
@@ -455,17 +464,18 @@ hipError_t launch_conv_input_grad(const uint16_t *grad_out, const uint16_t *w, c
     hipError_t e = train_workspace(wbytes + zbytes, &ws);
     if (e != hipSuccess) return e;
     uint16_t *wt = (uint16_t *)ws;
-    const int wtotal = fwd.cout * fwd.kh * fwd.kw * fwd.cin;
-    hipLaunchKernelGGL(k_flip_transpose16, dim3(blocks_for(wtotal)), dim3(kThreads), 0, s, w, wt,
-                       fwd.cout, fwd.kh, fwd.cin);
+    const unsigned wblocks = blocks_for((long long)fwd.cout * fwd.kh * fwd.kw * fwd.cin);
     const uint16_t *src = grad_out;
+    uint16_t *z = nullptr;
+    unsigned zblocks = 0;
     if (fwd.stride == 2) {
-        uint16_t *z = (uint16_t *)((uint8_t *)ws + wbytes);
-        const long long total = (long long)fwd.n * fwd.hin * fwd.win * (fwd.cout / 8);
-        hipLaunchKernelGGL(k_zero_insert16, dim3(blocks_for(total)), dim3(kThreads), 0, s,
-                           (const uint4 *)grad_out, (uint4 *)z, fwd.n, fwd.hout, fwd.wout, fwd.cout / 8);
+        z = (uint16_t *)((uint8_t *)ws + wbytes);
+        zblocks = blocks_for((long long)fwd.n * fwd.hin * fwd.win * (fwd.cout / 8));
         src = z;
     }
+    hipLaunchKernelGGL(k_input_grad_prep16, dim3(wblocks + zblocks), dim3(kThreads), 0, s, w, wt,
+                       fwd.cout, fwd.kh, fwd.cin, wblocks, (const uint4 *)grad_out, (uint4 *)z,
+                       fwd.n, fwd.hout, fwd.wout, fwd.cout / 8);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // stride-1 convolution of the (spread) output gradient with the flipped weights,
     // every block of the input-sized map (blocks of at most 8 x 8 pixels)

@@ -250,8 +250,9 @@ class PolicyNet:
             if l.res is not None:
                 acc = cur.get(l.res)
                 if acc is None:
-                    cur[l.res] = self.gbufs[l.res][0]
-                    bc.bc_grad_combine(gp, None, None, cur[l.res], stream)
+                    # the shortcut passes gp on unchanged; layer li's buffer is free from
+                    # here on and has l.res's shape, so it takes the sum in place
+                    cur[l.res] = gp
                 else:
                     bc.bc_grad_combine(acc, gp, None, acc, stream)
 
