@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 7
+#define BC_ABI_VERSION 8
 
 typedef enum {
     BC_OK = 0,
@@ -162,6 +162,35 @@ bc_status bc_sparse_conv2d(const bc_conv *conv,
                            void *d_out, bc_tensor out, bc_grid g,
                            const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
                            void *stream);
+
+/* The arguments of one bc_sparse_conv2d call (grid and index aside). */
+typedef struct bc_conv_call {
+    bc_conv conv;
+    const void *d_in;
+    bc_tensor in;
+    const void *d_w;
+    const float *d_bias;
+    const void *d_residual;
+    void *d_out;
+    bc_tensor out;
+} bc_conv_call;
+
+/*
+ * Two independent convolutions of one frame on the same execution grid and index:
+ * the same results, bit for bit, as bc_sparse_conv2d for *a followed by
+ * bc_sparse_conv2d for *b (every layer runs on the executed blocks only, Section 3.1).
+ * Meant for a residual block's shortcut projection and the first convolution of its
+ * branch, which read the same input: when both are NHWC BF16 1x1 layers, b at stride 1,
+ * and neither tile plan splits K, both run in one launch, one dependent launch fewer
+ * on the frame's chain; any other pair runs as two launches in order.
+ *   a, b   each call's arguments, checked as bc_sparse_conv2d checks them; neither
+ *          output may overlap any tensor of the other call (BC_ERR_ALIAS).
+ * Every check of both calls runs before anything is enqueued.
+ * Errors: those of bc_sparse_conv2d; BC_ERR_NULL if a or b is NULL.
+ */
+bc_status bc_sparse_conv2d_pair(const bc_conv_call *a, const bc_conv_call *b, bc_grid g,
+                                const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                void *stream);
 
 /*
  * Block-sparse max pooling (the ResNet stem pooling run block-sparsely), kernel

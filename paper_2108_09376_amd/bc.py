@@ -48,6 +48,12 @@ class bc_conv(ctypes.Structure):
                 ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
 
 
+class bc_conv_call(ctypes.Structure):
+    _fields_ = [("conv", bc_conv), ("d_in", ctypes.c_void_p), ("in_", bc_tensor),
+                ("d_w", ctypes.c_void_p), ("d_bias", ctypes.c_void_p),
+                ("d_residual", ctypes.c_void_p), ("d_out", ctypes.c_void_p), ("out", bc_tensor)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2108_09376_amd.build` "
                       "(there is no fallback path)")
@@ -64,6 +70,8 @@ _sigs = {
     "bc_scatter_blocks": ([_vp, _vp, _vp, _i32, bc_grid, _vp, bc_tensor, _vp], _i32),
     "bc_sparse_conv2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, _vp, bc_tensor,
                           bc_grid, _vp, _vp, _i32, _vp], _i32),
+    "bc_sparse_conv2d_pair": ([ctypes.POINTER(bc_conv_call), ctypes.POINTER(bc_conv_call), bc_grid,
+                               _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_maxpool2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, bc_grid, _vp,
                              _vp, _i32, _vp], _i32),
     "bc_fold_bn": ([_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp], _i32),
@@ -98,7 +106,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 7
+ABI_VERSION = 8
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -205,6 +213,23 @@ def bc_sparse_conv2d(conv, x, layout, w, bias, residual, out, grid, idx, count, 
                                _ptr(residual), _ptr(out), desc(out, layout), _grid(grid), _ptr(idx),
                                _ptr(count), cap, _stream(stream))
     _check(st, "bc_sparse_conv2d")
+
+
+def _call(conv, x, layout, w, bias, residual, out) -> bc_conv_call:
+    def addr(t):
+        return None if t is None else t.data_ptr()
+    return bc_conv_call(_conv(conv), addr(x), desc(x, layout), addr(w), addr(bias), addr(residual),
+                        addr(out), desc(out, layout))
+
+
+def bc_sparse_conv2d_pair(a, b, grid, idx, count, stream=None):
+    """Two independent convolutions on one grid and index; a and b are each the tuple
+    (conv, x, layout, w, bias, residual, out) of a bc_sparse_conv2d call."""
+    cap = 0 if idx is None else int(idx.numel())
+    ca, cb = _call(*a), _call(*b)
+    st = _lib.bc_sparse_conv2d_pair(ctypes.byref(ca), ctypes.byref(cb), _grid(grid), _ptr(idx),
+                                    _ptr(count), cap, _stream(stream))
+    _check(st, "bc_sparse_conv2d_pair")
 
 
 def bc_sparse_maxpool2d(geom, x, layout, out, grid, idx, count, stream=None):

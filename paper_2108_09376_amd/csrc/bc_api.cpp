@@ -336,13 +336,15 @@ static bc_status layer_common(const bc_conv *geom, bool conv, const void *d_in, 
     return BC_OK;
 }
 
-bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, const void *d_w,
-                           const float *d_bias, const void *d_residual, void *d_out, bc_tensor out,
-                           bc_grid g, const int32_t *d_idx, const int32_t *d_count,
-                           int32_t capacity, void *stream)
+namespace {
+
+// Every check of one convolution call, before anything is enqueued.
+bc_status conv_checks(const bc_conv *conv, const void *d_in, const bc_tensor &in, const void *d_w,
+                      const float *d_bias, const void *d_residual, void *d_out,
+                      const bc_tensor &out, const bc_grid &g, const int32_t *d_idx,
+                      const int32_t *d_count, int32_t capacity, LayerGeom &L)
 {
     if (!d_w) return fail(BC_ERR_NULL, "d_w is required");
-    LayerGeom L;
     bc_status st = layer_common(conv, true, d_in, in, d_out, out, g, d_idx, d_count, capacity, L);
     if (st) return st;
     const size_t wbytes = (size_t)out.c * in.c * conv->kh * conv->kw * esize_of(in.dtype);
@@ -359,8 +361,14 @@ bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, 
             return fail(BC_ERR_UNSUPPORTED, "fp32 path: output blocks above 2048 pixels or halo "
                                             "tiles above 48 KB per channel");
     }
-    if ((st = check_registered(d_out, out, d_idx != nullptr))) return st;
-    hipStream_t s = (hipStream_t)stream;
+    return check_registered(d_out, out, d_idx != nullptr);
+}
+
+bc_status conv_launch(const bc_conv *conv, const void *d_in, const bc_tensor &in, const void *d_w,
+                      const float *d_bias, const void *d_residual, void *d_out,
+                      const LayerGeom &L, hipStream_t s)
+{
+    const char *why = "";
     hipError_t e;
     if (in.layout == BC_NHWC) {
         e = bc::launch_conv_nhwc_mfma((const uint16_t *)d_in, (const uint16_t *)d_w, d_bias,
@@ -374,7 +382,77 @@ bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, 
     }
     if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
     if (e != hipSuccess) return hip_fail(e, "conv launch");
+    return BC_OK;
+}
+
+// Bytes of every tensor one call reads, for the cross-call alias checks.
+bool call_reads_overlap(const bc_conv_call &c, const void *p, size_t bytes)
+{
+    const size_t wbytes = (size_t)c.out.c * c.in.c * c.conv.kh * c.conv.kw * esize_of(c.in.dtype);
+    return overlap(p, bytes, c.d_in, tensor_bytes(c.in)) || overlap(p, bytes, c.d_w, wbytes) ||
+           overlap(p, bytes, c.d_bias, (size_t)c.out.c * 4) ||
+           overlap(p, bytes, c.d_residual, tensor_bytes(c.out)) ||
+           overlap(p, bytes, c.d_out, tensor_bytes(c.out));
+}
+
+}  // namespace
+
+bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, const void *d_w,
+                           const float *d_bias, const void *d_residual, void *d_out, bc_tensor out,
+                           bc_grid g, const int32_t *d_idx, const int32_t *d_count,
+                           int32_t capacity, void *stream)
+{
+    LayerGeom L;
+    bc_status st = conv_checks(conv, d_in, in, d_w, d_bias, d_residual, d_out, out, g, d_idx,
+                               d_count, capacity, L);
+    if (st) return st;
+    if ((st = conv_launch(conv, d_in, in, d_w, d_bias, d_residual, d_out, L, (hipStream_t)stream)))
+        return st;
     if (!d_idx) mark_full(d_out);
+    return ok();
+}
+
+bc_status bc_sparse_conv2d_pair(const bc_conv_call *a, const bc_conv_call *b, bc_grid g,
+                                const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                void *stream)
+{
+    if (!a || !b) return fail(BC_ERR_NULL, "both calls are required");
+    LayerGeom La, Lb;
+    bc_status st = conv_checks(&a->conv, a->d_in, a->in, a->d_w, a->d_bias, a->d_residual,
+                               a->d_out, a->out, g, d_idx, d_count, capacity, La);
+    if (st) return st;
+    if ((st = conv_checks(&b->conv, b->d_in, b->in, b->d_w, b->d_bias, b->d_residual, b->d_out,
+                          b->out, g, d_idx, d_count, capacity, Lb)))
+        return st;
+    if (call_reads_overlap(*b, a->d_out, tensor_bytes(a->out)))
+        return fail(BC_ERR_ALIAS, "the first call's output overlaps a tensor of the second");
+    if (call_reads_overlap(*a, b->d_out, tensor_bytes(b->out)))
+        return fail(BC_ERR_ALIAS, "the second call's output overlaps a tensor of the first");
+    hipStream_t s = (hipStream_t)stream;
+    if (a->in.layout == BC_NHWC && b->in.layout == BC_NHWC && a->in.dtype == b->in.dtype) {
+        const bc::ConvCall ca{(const uint16_t *)a->d_in, (const uint16_t *)a->d_w,
+                              (const uint16_t *)a->d_residual, a->d_bias, (uint16_t *)a->d_out,
+                              a->conv.relu, La};
+        const bc::ConvCall cb{(const uint16_t *)b->d_in, (const uint16_t *)b->d_w,
+                              (const uint16_t *)b->d_residual, b->d_bias, (uint16_t *)b->d_out,
+                              b->conv.relu, Lb};
+        const char *why = "";
+        const hipError_t e = bc::launch_conv_pair_nhwc_mfma(
+            ca, cb, a->in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16, s, &why);
+        if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
+        if (e != hipSuccess) return hip_fail(e, "conv pair launch");
+    } else {
+        if ((st = conv_launch(&a->conv, a->d_in, a->in, a->d_w, a->d_bias, a->d_residual, a->d_out,
+                              La, s)))
+            return st;
+        if ((st = conv_launch(&b->conv, b->d_in, b->in, b->d_w, b->d_bias, b->d_residual, b->d_out,
+                              Lb, s)))
+            return st;
+    }
+    if (!d_idx) {
+        mark_full(a->d_out);
+        mark_full(b->d_out);
+    }
     return ok();
 }
 

@@ -44,6 +44,17 @@ hipError_t launch_conv_nchw_f32(const float *x, const float *w, const float *bia
 hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const float *bias,
                                  const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
                                  const LayerGeom &g, hipStream_t s, const char **why);
+// Two independent channels-last layers: one launch when both are 1x1 layers whose plans
+// pair (the second at stride 1, neither splitting K, BF16), else one launch each.
+struct ConvCall {
+    const uint16_t *x, *w, *res;
+    const float *bias;
+    uint16_t *y;
+    int relu;
+    LayerGeom g;
+};
+hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Half16 fmt,
+                                      hipStream_t s, const char **why);
 // Host-side check used by the ABI validation before anything is enqueued.
 bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why);
 

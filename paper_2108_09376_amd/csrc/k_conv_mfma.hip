@@ -569,8 +569,9 @@ __device__ __forceinline__ void ring_loop(F &f, int n)
 
 // SG (stage grouping) sets how much of K one barrier covers: one tap (SG = 1), all KT
 // taps of a 32-channel chunk (SG = KT, 3x3 layers), or two chunks (SG = 2, 1x1 layers).
+// One workgroup's tile L of the launch grid (the kernels below give it blockIdx.x).
 template <bool BF16, int BM, int BN, int KS, int S, int SG>
-__global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
+__device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
 {
     constexpr int SS = (KS == 1) ? S : 1;
     constexpr int ST = S / SS;
@@ -587,7 +588,6 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     const int wm = wave >> 1, wn = wave & 1, q = tid & 3;
     // natural tile order L = (mt * ntn + nt) * ksplit + ks: N tile and K slice are known
     // without the active count
-    const int L = blockIdx.x;
     const int ks = L % a.ksplit;
     const int mn = L / a.ksplit;
     const int nt = mn % a.ntn;
@@ -782,6 +782,26 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
     if constexpr (BM == 64 && BN == 64)
         if (a.ksplit > 1 && !split_k_handoff(a, acc, mt * a.ntn + nt, ks, &s_last)) return;
     epi.finish(a, acc, smem, n0);
+}
+
+template <bool BF16, int BM, int BN, int KS, int S, int SG>
+__global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
+{
+    conv_pipe_tile<BF16, BM, BN, KS, S, SG>(a, blockIdx.x);
+}
+
+// Two independent 1x1 layers of one frame in one launch (a block's shortcut projection
+// and the first convolution of its residual branch read the same input): workgroups
+// below grid1 run tiles of the first layer, the rest tiles of the second (stride 1).
+// Each tile runs exactly as in its own launch, so results are the same bits; neither
+// layer may split K (the split counters and workspace are per launch).
+template <bool BF16, int BN1, int S1, int SG1, int BN2, int SG2>
+__global__ __launch_bounds__(kThreads) void k_conv_pipe_pair(MfmaArgs a1, MfmaArgs a2, int grid1)
+{
+    if ((int)blockIdx.x < grid1)
+        conv_pipe_tile<BF16, 64, BN1, 1, S1, SG1>(a1, blockIdx.x);
+    else
+        conv_pipe_tile<BF16, 64, BN2, 1, 1, SG2>(a2, (int)blockIdx.x - grid1);
 }
 
 // ------------------------------------------------------------------ stem form
@@ -1374,12 +1394,12 @@ bool conv_nhwc_mfma_supported(const LayerGeom &g, const char **why)
     return true;
 }
 
-hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const float *bias,
-                                 const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
-                                 const LayerGeom &g, hipStream_t s, const char **why)
+namespace {
+
+// The plan of one channels-last layer with its arguments filled in (no launch).
+void fill_plan(const uint16_t *x, const uint16_t *w, const float *bias, const uint16_t *res,
+               uint16_t *y, int relu, const LayerGeom &g, Plan &p)
 {
-    if (!conv_nhwc_mfma_supported(g, why)) return hipErrorInvalidValue;
-    Plan p;
     choose_plan(g, p);
     MfmaArgs &a = p.a;
     a.x = x; a.w = w; a.bias = bias; a.res = res; a.y = y;
@@ -1401,15 +1421,79 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     }
     a.f_rbw = make_fastdiv(a.R * g.bw);
     a.f_bw = make_fastdiv(g.bw);
+}
+
+hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s)
+{
     if (p.grid == 0) return hipSuccess;
     if (p.ws_bytes) {
-        hipError_t e = workspace(p.ws_bytes, &a.ws);
+        hipError_t e = workspace(p.ws_bytes, &p.a.ws);
         if (e != hipSuccess) return e;
     }
     const hipError_t e = fmt == Half16::BF16 ? launch_geom<true>(p, g.kh, g.stride, s)
                                              : launch_geom<false>(p, g.kh, g.stride, s);
     if (e != hipSuccess) return e;
     return hipGetLastError();
+}
+
+// The (tile width, stage grouping) variants of 64-row 1x1 pipelined plans: 0 = 64 wide,
+// two chunks per barrier; 1 = 128 wide, one chunk; -1 = another form.
+int pair_variant(const Plan &p)
+{
+    if (p.form != Form::Pipe || p.BM != 64 || p.a.ksplit != 1) return -1;
+    if (p.BN == 64 && p.sg == 2) return 0;
+    if (p.BN == 128 && p.sg == 1) return 1;
+    return -1;
+}
+
+template <int BN1, int S1, int SG1>
+hipError_t launch_pair_second(const Plan &p1, const Plan &p2, int v2, hipStream_t s)
+{
+    const size_t lds = p1.lds > p2.lds ? p1.lds : p2.lds;
+    const unsigned grid = p1.grid + p2.grid;
+    if (v2 == 0)
+        hipLaunchKernelGGL((k_conv_pipe_pair<true, BN1, S1, SG1, 64, 2>), dim3(grid),
+                           dim3(kThreads), lds, s, p1.a, p2.a, (int)p1.grid);
+    else
+        hipLaunchKernelGGL((k_conv_pipe_pair<true, BN1, S1, SG1, 128, 1>), dim3(grid),
+                           dim3(kThreads), lds, s, p1.a, p2.a, (int)p1.grid);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const float *bias,
+                                 const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
+                                 const LayerGeom &g, hipStream_t s, const char **why)
+{
+    if (!conv_nhwc_mfma_supported(g, why)) return hipErrorInvalidValue;
+    Plan p;
+    fill_plan(x, w, bias, res, y, relu, g, p);
+    return launch_plan(p, fmt, g, s);
+}
+
+hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Half16 fmt,
+                                      hipStream_t s, const char **why)
+{
+    if (!conv_nhwc_mfma_supported(c1.g, why) || !conv_nhwc_mfma_supported(c2.g, why))
+        return hipErrorInvalidValue;
+    Plan p1, p2;
+    fill_plan(c1.x, c1.w, c1.bias, c1.res, c1.y, c1.relu, c1.g, p1);
+    fill_plan(c2.x, c2.w, c2.bias, c2.res, c2.y, c2.relu, c2.g, p2);
+    const int v1 = pair_variant(p1), v2 = pair_variant(p2);
+    if (fmt == Half16::BF16 && c1.g.kh == 1 && c2.g.kh == 1 && c2.g.stride == 1 && v1 >= 0 &&
+        v2 >= 0 && p1.grid > 0 && p2.grid > 0 && (size_t)p1.grid + p2.grid < (1u << 31) &&
+        p1.lds < 60 * 1024 && p2.lds < 60 * 1024) {   // no dynamic-LDS opt-in needed
+        if (c1.g.stride == 1)
+            return v1 == 0 ? launch_pair_second<64, 1, 2>(p1, p2, v2, s)
+                           : launch_pair_second<128, 1, 1>(p1, p2, v2, s);
+        return v1 == 0 ? launch_pair_second<64, 2, 2>(p1, p2, v2, s)
+                       : launch_pair_second<128, 2, 1>(p1, p2, v2, s);
+    }
+    // any other pair: one launch per layer, in order
+    hipError_t e = launch_plan(p1, fmt, c1.g, s);
+    if (e != hipSuccess) return e;
+    return launch_plan(p2, fmt, c2.g, s);
 }
 
 }  // namespace bc

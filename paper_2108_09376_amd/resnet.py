@@ -332,6 +332,8 @@ class SparseResNet:
         self.idx = torch.zeros(nblk, dtype=torch.int32, device=self.device)
         self.count = torch.zeros(1, dtype=torch.int32, device=self.device)
         self.mask = torch.zeros((1,) + self.grid, dtype=torch.uint8, device=self.device)
+        self.pairs = self._find_pairs()
+        self.pair_launches = True
 
     # ------------------------------------------------------------------
     def conv_flops(self, active_blocks: int) -> float:
@@ -364,9 +366,39 @@ class SparseResNet:
             idx, cnt = self.idx, self.count
         else:
             idx = cnt = None
-        for i, l in enumerate(self.layers):
-            self.run_layer(i, x, idx, cnt, stream)
+        i = 0
+        while i < len(self.layers):
+            if self.pair_launches and i in self.pairs:
+                self.run_pair(i, x, idx, cnt, stream)
+                i += 2
+            else:
+                self.run_layer(i, x, idx, cnt, stream)
+                i += 1
         return self.buffers[-1]
+
+    def _find_pairs(self) -> set[int]:
+        """Layers i whose successor i + 1 is independent of it and pairs with it in one
+        launch: both 1x1 convolutions of one input (a block's shortcut projection and
+        its branch's first convolution), the second at stride 1."""
+        out = set()
+        for i in range(len(self.layers) - 1):
+            a, b = self.layers[i], self.layers[i + 1]
+            if (a.kind == b.kind == "conv" and a.k == b.k == 1 and a.src == b.src
+                    and b.stride == 1 and b.res != i and (i - 1) not in out):
+                out.add(i)
+        return out
+
+    def _call(self, i, x):
+        l = self.layers[i]
+        src = x if l.src < 0 else self.buffers[l.src]
+        res = None if l.res is None else self.buffers[l.res]
+        return ((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC, self.weights[i],
+                self.biases[i], res, self.buffers[i])
+
+    def run_pair(self, i, x, idx, cnt, stream=None):
+        """Layers i and i + 1 (see _find_pairs) through one library call."""
+        bc.bc_sparse_conv2d_pair(self._call(i, x), self._call(i + 1, x), self.grid, idx, cnt,
+                                 stream)
 
     def run_layer(self, i, x, idx, cnt, stream=None):
         l = self.layers[i]

@@ -31,7 +31,7 @@ def test_header_declares_the_boundary():
               "bc_sample_execution_grid", "bc_update_frame_state", "bc_seg_information_gain",
               "bc_block_rewards", "bc_sparse_upsample_add", "bc_policy_input", "bc_policy_probabilities",
               "bc_policy_logit_grad", "bc_grad_combine", "bc_conv2d_input_grad", "bc_conv2d_weight_grad",
-              "bc_rmsprop_step", "bc_rmsprop_step_many"]:
+              "bc_rmsprop_step", "bc_rmsprop_step_many", "bc_sparse_conv2d_pair"]:
         assert n in names
 
 
@@ -106,6 +106,48 @@ def test_conv_validation_codes(B):
     assert conv_call(B, inp=(1, 16, 64, 128, 0, 1), out=(1, 16, 64, 128, 0, 1))[0] == E.BC_ERR_UNSUPPORTED
     assert conv_call(B, inp=(1, 16, 64, 128, 0, 0), out=(1, 16, 64, 128, 0, 0), grid=(1, 1))[0] == E.BC_ERR_UNSUPPORTED
     assert B.bc_last_error()
+
+
+FAKE_IN2, FAKE_W2, FAKE_OUT2 = 0x70000000, 0x74000000, 0x78000000
+
+
+def pair_call(B, a=None, b=None, grid=(8, 16), d_idx=FAKE_IDX, d_cnt=FAKE_CNT, cap=128, null=None):
+    """A valid-looking 1x1 shortcut + 1x1 branch pair on fake addresses; a and b override
+    bc_conv_call fields of either call."""
+    lib = B.raw()
+    t = (1, 64, 64, 128, 1, 1)
+    ca = B.bc_conv_call(B.bc_conv(1, 1, 1, 0, 0), FAKE_IN, B.bc_tensor(*t), FAKE_W, None, None,
+                        FAKE_OUT, B.bc_tensor(1, 256, 64, 128, 1, 1))
+    cb = B.bc_conv_call(B.bc_conv(1, 1, 1, 0, 1), FAKE_IN, B.bc_tensor(*t), FAKE_W2, None, None,
+                        FAKE_OUT2, B.bc_tensor(*t))
+    for c, over in ((ca, a or {}), (cb, b or {})):
+        for k, v in over.items():
+            setattr(c, k, v)
+    pa = None if null == "a" else ctypes.byref(ca)
+    pb = None if null == "b" else ctypes.byref(cb)
+    st = lib.bc_sparse_conv2d_pair(pa, pb, B.bc_grid(*grid), d_idx, d_cnt, cap, None)
+    return st, B.bc_last_error()
+
+
+@no_gpu
+def test_conv_pair_validation_codes(B):
+    """Both calls are checked as bc_sparse_conv2d checks them, then against each other;
+    every case fails before anything is enqueued (fake addresses)."""
+    E = B
+    assert pair_call(B, null="a")[0] == E.BC_ERR_NULL
+    assert pair_call(B, null="b")[0] == E.BC_ERR_NULL
+    assert pair_call(B, b={"d_w": None})[0] == E.BC_ERR_NULL
+    assert pair_call(B, a={"out": B.bc_tensor(1, 256, 32, 128, 1, 1)})[0] == E.BC_ERR_SHAPE
+    assert pair_call(B, b={"out": B.bc_tensor(1, 48, 64, 128, 1, 1)})[0] == E.BC_ERR_UNSUPPORTED
+    assert pair_call(B, cap=127)[0] == E.BC_ERR_CAPACITY
+    st, msg = pair_call(B, b={"d_out": FAKE_OUT + 64})          # outputs overlap
+    assert st == E.BC_ERR_ALIAS and "second" in msg
+    st, msg = pair_call(B, b={"d_residual": FAKE_OUT})          # b reads a's output
+    assert st == E.BC_ERR_ALIAS and "first call's output" in msg
+    st, msg = pair_call(B, a={"d_residual": FAKE_OUT2 + 2})     # a reads b's output
+    assert st == E.BC_ERR_ALIAS and "second call's output" in msg
+    st, msg = pair_call(B, a={"d_w": FAKE_OUT2})                # a's weights inside b's output
+    assert st == E.BC_ERR_ALIAS
 
 
 @no_gpu
