@@ -366,26 +366,39 @@ class SparseResNet:
             idx, cnt = self.idx, self.count
         else:
             idx = cnt = None
-        i = 0
-        while i < len(self.layers):
-            if self.pair_launches and i in self.pairs:
-                self.run_pair(i, x, idx, cnt, stream)
-                i += 2
-            else:
+        done = set()
+        for i in range(len(self.layers)):
+            if i in done:
+                continue
+            j = self.pairs.get(i) if self.pair_launches else None
+            if j is None:
                 self.run_layer(i, x, idx, cnt, stream)
-                i += 1
+            else:
+                self.run_pair(i, j, x, idx, cnt, stream)
+                done.add(j)
         return self.buffers[-1]
 
-    def _find_pairs(self) -> set[int]:
-        """Layers i whose successor i + 1 is independent of it and pairs with it in one
-        launch: both 1x1 convolutions of one input (a block's shortcut projection and
-        its branch's first convolution), the second at stride 1."""
-        out = set()
-        for i in range(len(self.layers) - 1):
-            a, b = self.layers[i], self.layers[i + 1]
-            if (a.kind == b.kind == "conv" and a.k == b.k == 1 and a.src == b.src
-                    and b.stride == 1 and b.res != i and (i - 1) not in out):
-                out.add(i)
+    def _find_pairs(self) -> dict[int, int]:
+        """{i: j}: layer j > i runs in one launch with layer i, at i's turn. Both are 1x1
+        convolutions (j at stride 1) and independent: j reads only layers before i (so
+        moving it forward changes nothing it reads) and nothing between them reads j,
+        which only later layers can. Found greedily: a block's shortcut projection with
+        its branch's first convolution; a decoder's lateral projections with each other."""
+        L, out, taken = self.layers, {}, set()
+
+        def one_by_one(l):
+            return l.kind == "conv" and l.k == 1
+
+        for i, a in enumerate(L):
+            if i in taken or not one_by_one(a):
+                continue
+            for j in range(i + 1, len(L)):
+                b = L[j]
+                if (j not in taken and one_by_one(b) and b.stride == 1 and b.src < i
+                        and (b.res is None or b.res < i)):
+                    out[i] = j
+                    taken.update((i, j))
+                    break
         return out
 
     def _call(self, i, x):
@@ -395,10 +408,9 @@ class SparseResNet:
         return ((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC, self.weights[i],
                 self.biases[i], res, self.buffers[i])
 
-    def run_pair(self, i, x, idx, cnt, stream=None):
-        """Layers i and i + 1 (see _find_pairs) through one library call."""
-        bc.bc_sparse_conv2d_pair(self._call(i, x), self._call(i + 1, x), self.grid, idx, cnt,
-                                 stream)
+    def run_pair(self, i, j, x, idx, cnt, stream=None):
+        """Layers i and j (see _find_pairs) through one library call."""
+        bc.bc_sparse_conv2d_pair(self._call(i, x), self._call(j, x), self.grid, idx, cnt, stream)
 
     def run_layer(self, i, x, idx, cnt, stream=None):
         l = self.layers[i]
