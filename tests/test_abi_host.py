@@ -401,3 +401,32 @@ def test_runner_table_matches_oracle_table():
         for x, y in zip(a, b):
             assert (x["kind"], x["cin"], x["cout"], x["k"], x["stride"], x["pad"], x["relu"], x["src"], x["res"]) == \
                    (y.kind, y.cin, y.cout, y.k, y.stride, y.pad, y.relu, y.src, y.res), (x["name"], y.name)
+
+
+def test_runner_pairs_independent_layers_only():
+    """Layers the frame runner launches together: two 1x1 convolutions, the second at
+    stride 1 and reading only layers before the first (so running it early changes
+    nothing it reads, and the first never reads it); every layer in at most one pair."""
+    from paper_2108_09376_amd import resnet
+
+    class Table:
+        def __init__(self, layers):
+            self.layers = layers
+
+    tables = {"r50": resnet.build_layers(50), "r18": resnet.build_layers(18),
+              "swift18": resnet.build_swiftnet_layers(18), "swift50": resnet.build_swiftnet_layers(50)}
+    found = {}
+    for name, L in tables.items():
+        pairs = resnet.SparseResNet._find_pairs(Table(L))
+        found[name] = pairs
+        members = list(pairs) + list(pairs.values())
+        assert len(members) == len(set(members)), name
+        for i, j in pairs.items():
+            a, b = L[i], L[j]
+            assert i < j and a.kind == b.kind == "conv" and a.k == b.k == 1 and b.stride == 1
+            assert b.src < i and (b.res is None or b.res < i), (name, a.name, b.name)
+            assert all(l.src != j and l.res != j for l in L[i:j]), (name, b.name)
+    r50 = tables["r50"]
+    assert sorted((r50[i].name, r50[j].name) for i, j in found["r50"].items()) == [
+        (f"layer{s}.0.downsample", f"layer{s}.0.conv1") for s in (1, 2, 3, 4)]
+    assert not found["r18"]                    # its shortcuts pair with 3x3 layers only
