@@ -179,10 +179,11 @@ typedef struct bc_conv_call {
  * Two independent convolutions of one frame on the same execution grid and index:
  * the same results, bit for bit, as bc_sparse_conv2d for *a followed by
  * bc_sparse_conv2d for *b (every layer runs on the executed blocks only, Section 3.1).
- * Meant for a residual block's shortcut projection and the first convolution of its
- * branch, which read the same input: when both are NHWC BF16 1x1 layers, b at stride 1,
- * and neither tile plan splits K, both run in one launch, one dependent launch fewer
- * on the frame's chain; any other pair runs as two launches in order.
+ * Meant for independent layers of one frame, such as a residual block's shortcut
+ * projection and the first convolution of its branch (one input), or a decoder's
+ * lateral projection and an encoder layer: when both are NHWC BF16 1x1 layers, b at
+ * stride 1, and neither tile plan splits K, both run in one launch, one dependent
+ * launch fewer on the frame's chain; any other pair runs as two launches in order.
  *   a, b   each call's arguments, checked as bc_sparse_conv2d checks them; neither
  *          output may overlap any tensor of the other call (BC_ERR_ALIAS).
  * Every check of both calls runs before anything is enqueued.
