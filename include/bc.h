@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 8
+#define BC_ABI_VERSION 9
 
 typedef enum {
     BC_OK = 0,
@@ -63,7 +63,9 @@ typedef enum {
     BC_ERR_ALIAS = 7,         /* output overlaps an input                        */
     BC_ERR_UNINITIALIZED = 8, /* sparse write into a registered, invalid buffer  */
     BC_ERR_UNSUPPORTED = 9,   /* valid request outside what the kernels implement */
-    BC_ERR_HIP = 10           /* HIP runtime error (launch or earlier async fault) */
+    BC_ERR_HIP = 10,          /* HIP runtime error (launch or earlier async fault) */
+    BC_ERR_CAPTURE = 11       /* a library allocation was needed while the stream is
+                                 capturing a graph; nothing was enqueued            */
 } bc_status;
 
 typedef enum { BC_F32 = 0, BC_BF16 = 1, BC_F16 = 2 } bc_dtype;
@@ -155,6 +157,23 @@ bc_status bc_scatter_blocks(const void *d_packed, const int32_t *d_idx, const in
  * If d_out is a registered buffer (bc_buffer_register) that is not valid, a sparse
  * call (d_idx non-NULL) returns BC_ERR_UNINITIALIZED; a full call (d_idx = d_count
  * = NULL) makes it valid.
+ * Library state used by NHWC calls whose layer splits K over several workgroups (the
+ * tile plan depends on the layer's shape and grid only; it splits for few full-frame
+ * tiles with a long K, e.g. the stride-32 layers of a ResNet at 2048x1024):
+ *  - a split-K workspace of 64 MiB per device (fp32 partial tiles), owned by the
+ *    library, allocated by the first such call on the device and never freed or
+ *    moved (a captured graph keeps a valid pointer whatever runs later). That first
+ *    allocation is refused with BC_ERR_CAPTURE if the stream is capturing a graph:
+ *    make one uncaptured call of such a layer first;
+ *  - per-tile arrival counters in a static device array; the last K slice of a tile
+ *    resets its counter, so no clearing is needed between calls or graph replays.
+ * Both are shared by every call on a device: calls on one device must not overlap
+ * in time (use one stream, or order the streams with events). Calls that do not
+ * split K use neither. Results never depend on the plan's split: slices are added in
+ * a fixed order, so an active block's output bits do not depend on the other blocks.
+ * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT,
+ * BC_ERR_NOT_DIVISIBLE, BC_ERR_CAPACITY, BC_ERR_ALIAS, BC_ERR_UNINITIALIZED,
+ * BC_ERR_UNSUPPORTED, BC_ERR_CAPTURE, BC_ERR_HIP.
  */
 bc_status bc_sparse_conv2d(const bc_conv *conv,
                            const void *d_in, bc_tensor in,
@@ -414,11 +433,12 @@ bc_status bc_grad_combine(const void *d_a, const void *d_b, const void *d_y, bc_
  * the matrix-core convolution with flipped, transposed weights (and for stride 2 the
  * output gradient spread onto even pixels) in a library-owned workspace, one per
  * device, used in stream order (calls on different streams of one device race). The
- * workspace grows (hipFree + hipMalloc) when a call needs more than it holds: a
- * caller that captures calls into a graph makes one eager call at the largest size
- * first, so no capture allocates and no captured pointer is freed later.
+ * workspace grows when a call needs more than it holds, by allocating a larger
+ * buffer; earlier buffers are kept until the process ends, so a captured graph never
+ * holds a freed pointer. Growth is refused with BC_ERR_CAPTURE while the stream is
+ * capturing: a caller that captures makes one eager call at the largest size first.
  * Errors: BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_ALIAS
- * (d_grad_in overlapping an input), BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ * (d_grad_in overlapping an input), BC_ERR_UNSUPPORTED, BC_ERR_CAPTURE, BC_ERR_HIP.
  */
 bc_status bc_conv2d_input_grad(const bc_conv *geom, const void *d_grad_out, bc_tensor grad_out,
                                const void *d_w, const void *d_accum, void *d_grad_in,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libblockcopy.so")
 
 BC_OK, BC_ERR_NULL, BC_ERR_SHAPE, BC_ERR_DTYPE, BC_ERR_LAYOUT = 0, 1, 2, 3, 4
 BC_ERR_NOT_DIVISIBLE, BC_ERR_CAPACITY, BC_ERR_ALIAS, BC_ERR_UNINITIALIZED = 5, 6, 7, 8
-BC_ERR_UNSUPPORTED, BC_ERR_HIP = 9, 10
+BC_ERR_UNSUPPORTED, BC_ERR_HIP, BC_ERR_CAPTURE = 9, 10, 11
 BC_F32, BC_BF16, BC_F16 = 0, 1, 2
 BC_NCHW, BC_NHWC = 0, 1
 
@@ -106,7 +106,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 8
+ABI_VERSION = 9
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")

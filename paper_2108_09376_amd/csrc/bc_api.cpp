@@ -179,6 +179,7 @@ const char *bc_status_str(int32_t s)
     case BC_ERR_UNINITIALIZED: return "sparse write into an invalid buffer";
     case BC_ERR_UNSUPPORTED: return "unsupported configuration";
     case BC_ERR_HIP: return "HIP runtime error";
+    case BC_ERR_CAPTURE: return "allocation refused while the stream is capturing";
     default: return "unknown status";
     }
 }
@@ -364,6 +365,15 @@ bc_status conv_checks(const bc_conv *conv, const void *d_in, const bc_tensor &in
     return check_registered(d_out, out, d_idx != nullptr);
 }
 
+// Status of a failed convolution launch: a refused capture, a shape the kernels do not
+// take (with the reason), or a HIP error.
+bc_status conv_fail(hipError_t e, const char *why, const char *what)
+{
+    if (e == hipErrorStreamCaptureUnsupported && why && *why) return fail(BC_ERR_CAPTURE, "%s", why);
+    if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
+    return hip_fail(e, what);
+}
+
 bc_status conv_launch(const bc_conv *conv, const void *d_in, const bc_tensor &in, const void *d_w,
                       const float *d_bias, const void *d_residual, void *d_out,
                       const LayerGeom &L, hipStream_t s)
@@ -380,8 +390,7 @@ bc_status conv_launch(const bc_conv *conv, const void *d_in, const bc_tensor &in
                                      (const float *)d_residual, (float *)d_out, conv->relu, L, s,
                                      &why);
     }
-    if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
-    if (e != hipSuccess) return hip_fail(e, "conv launch");
+    if (e != hipSuccess) return conv_fail(e, why, "conv launch");
     return BC_OK;
 }
 
@@ -439,8 +448,7 @@ bc_status bc_sparse_conv2d_pair(const bc_conv_call *a, const bc_conv_call *b, bc
         const char *why = "";
         const hipError_t e = bc::launch_conv_pair_nhwc_mfma(
             ca, cb, a->in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16, s, &why);
-        if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
-        if (e != hipSuccess) return hip_fail(e, "conv pair launch");
+        if (e != hipSuccess) return conv_fail(e, why, "conv pair launch");
     } else {
         if ((st = conv_launch(&a->conv, a->d_in, a->in, a->d_w, a->d_bias, a->d_residual, a->d_out,
                               La, s)))
@@ -869,8 +877,7 @@ bc_status bc_conv2d_input_grad(const bc_conv *geom, const void *d_grad_out, bc_t
         (const uint16_t *)d_grad_out, (const uint16_t *)d_w, (const uint16_t *)d_accum,
         (uint16_t *)d_grad_in, L, grad_in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16,
         (hipStream_t)stream, &why);
-    if (e == hipErrorInvalidValue && why && *why) return fail(BC_ERR_UNSUPPORTED, "%s", why);
-    if (e != hipSuccess) return hip_fail(e, "input gradient launch");
+    if (e != hipSuccess) return conv_fail(e, why, "input gradient launch");
     return ok();
 }
 

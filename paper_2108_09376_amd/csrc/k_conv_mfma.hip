@@ -34,8 +34,6 @@
 // 7x7 RGB stem): K is ordered (kernel row i, then the kw*Cin values of that row,
 // which are contiguous in a channels-last row), one MFMA k step per kernel row.
 #include <mutex>
-#include <map>
-#include <set>
 #include <type_traits>
 
 #include "bc_internal.h"
@@ -793,8 +791,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 // Two independent 1x1 layers of one frame in one launch (a block's shortcut projection
 // and the first convolution of its residual branch read the same input): workgroups
 // below grid1 run tiles of the first layer, the rest tiles of the second (stride 1).
-// Each tile runs exactly as in its own launch, so results are the same bits; neither
-// layer may split K (the split counters and workspace are per launch).
+// Each tile runs exactly as in its own launch, so results are the same bits. Neither
+// layer may split K: both would index the same per-tile counters and partials, which
+// one launch of one layer owns.
 template <bool BF16, int BN1, int S1, int SG1, int BN2, int SG2>
 __global__ __launch_bounds__(kThreads) void k_conv_pipe_pair(MfmaArgs a1, MfmaArgs a2, int grid1)
 {
@@ -1263,40 +1262,55 @@ bool choose_plan(const LayerGeom &g, Plan &best)
     return have;
 }
 
-// Split-K workspace: one per device, grown on demand (never during a call that is
-// being captured into a graph if the first uncaptured call already sized it).
+// Split-K partials. A plan splits K only for layers with at most 2048 full-frame tiles
+// (two slices) or at most 256 (up to four), so one call needs at most
+// 2048 * 2 * 64 * 64 * 4 bytes = 64 MiB (choose_plan; checked again in launch_plan).
+constexpr size_t kWorkspaceBytes = (size_t)64 << 20;
+
+// bc_sparse_conv2d: a library-owned workspace of kWorkspaceBytes per device, allocated by
+// the first call that splits K and never freed or moved, so a graph that captured a
+// split call keeps a valid pointer whatever runs later. hipMalloc is not allowed while
+// the stream is capturing: a capturing call that would allocate is refused (a prior
+// uncaptured split call on the device avoids that).
 std::mutex g_ws_mu;
 void *g_ws_ptr[64];
-size_t g_ws_bytes[64];
 
-hipError_t workspace(size_t bytes, float **out)
+hipError_t workspace(hipStream_t s, float **out, const char **why)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
     std::lock_guard<std::mutex> lk(g_ws_mu);
-    if (g_ws_bytes[dev] < bytes) {
-        const size_t want = bytes < ((size_t)64 << 20) ? ((size_t)64 << 20) : bytes;
-        if (g_ws_ptr[dev]) {
-            e = hipFree(g_ws_ptr[dev]);
-            g_ws_ptr[dev] = nullptr;
-            g_ws_bytes[dev] = 0;
-            if (e != hipSuccess) return e;
+    if (!g_ws_ptr[dev]) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(s, &cs);
+        if (e != hipSuccess) return e;
+        if (cs != hipStreamCaptureStatusNone) {
+            *why = "the split-K workspace of this device is not allocated yet and the stream is "
+                   "capturing (no allocation during capture): make one uncaptured call that "
+                   "splits K first";
+            return hipErrorStreamCaptureUnsupported;
         }
-        e = hipMalloc(&g_ws_ptr[dev], want);
-        if (e != hipSuccess) {
-            g_ws_ptr[dev] = nullptr;
-            return e;
-        }
-        g_ws_bytes[dev] = want;
+        void *p = nullptr;
+        e = hipMalloc(&p, kWorkspaceBytes);
+        if (e != hipSuccess) return e;
+        g_ws_ptr[dev] = p;
     }
     *out = (float *)g_ws_ptr[dev];
     return hipSuccess;
 }
 
+// Dynamic LDS each kernel has opted in to: a fixed table (a launch allocates no host
+// memory either); the library has a few dozen kernel instantiations.
+struct LdsOptIn {
+    const void *fn;
+    size_t lds;
+};
+constexpr int kMaxOptIn = 256;
 std::mutex g_attr_mu;
-std::map<const void *, size_t> g_attr_lds;   // dynamic LDS each kernel has opted in to
+LdsOptIn g_attr_lds[kMaxOptIn];
+int g_attr_n = 0;
 
 template <typename K>
 hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
@@ -1305,12 +1319,17 @@ hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
         // opt in to 60 KB or more of dynamic LDS (gfx950: 160 KB per workgroup, static
         // shared memory included), raised per kernel to the largest size launched so far
         std::lock_guard<std::mutex> lk(g_attr_mu);
-        size_t &cur = g_attr_lds[(const void *)kernel];
-        if (cur < p.lds) {
+        int i = 0;
+        while (i < g_attr_n && g_attr_lds[i].fn != (const void *)kernel) ++i;
+        if (i == g_attr_n) {
+            if (g_attr_n == kMaxOptIn) return hipErrorOutOfMemory;
+            g_attr_lds[g_attr_n++] = LdsOptIn{(const void *)kernel, 0};
+        }
+        if (g_attr_lds[i].lds < p.lds) {
             const hipError_t e = hipFuncSetAttribute(
                 (const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
             if (e != hipSuccess) return e;
-            cur = p.lds;
+            g_attr_lds[i].lds = p.lds;
         }
     }
     hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads), p.lds, s, p.a);
@@ -1423,11 +1442,15 @@ void fill_plan(const uint16_t *x, const uint16_t *w, const float *bias, const ui
     a.f_bw = make_fastdiv(g.bw);
 }
 
-hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s)
+hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s, const char **why)
 {
     if (p.grid == 0) return hipSuccess;
     if (p.ws_bytes) {
-        hipError_t e = workspace(p.ws_bytes, &p.a.ws);
+        if (p.ws_bytes > kWorkspaceBytes) {
+            *why = "split-K partials larger than the workspace";
+            return hipErrorInvalidValue;
+        }
+        const hipError_t e = workspace(s, &p.a.ws, why);
         if (e != hipSuccess) return e;
     }
     const hipError_t e = fmt == Half16::BF16 ? launch_geom<true>(p, g.kh, g.stride, s)
@@ -1469,7 +1492,7 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     if (!conv_nhwc_mfma_supported(g, why)) return hipErrorInvalidValue;
     Plan p;
     fill_plan(x, w, bias, res, y, relu, g, p);
-    return launch_plan(p, fmt, g, s);
+    return launch_plan(p, fmt, g, s, why);
 }
 
 hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Half16 fmt,
@@ -1491,9 +1514,9 @@ hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Ha
                        : launch_pair_second<128, 2, 1>(p1, p2, v2, s);
     }
     // any other pair: one launch per layer, in order
-    hipError_t e = launch_plan(p1, fmt, c1.g, s);
+    hipError_t e = launch_plan(p1, fmt, c1.g, s, why);
     if (e != hipSuccess) return e;
-    return launch_plan(p2, fmt, c2.g, s);
+    return launch_plan(p2, fmt, c2.g, s, why);
 }
 
 }  // namespace bc

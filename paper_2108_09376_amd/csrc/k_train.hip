@@ -393,11 +393,15 @@ __global__ __launch_bounds__(kThreads) void k_rmsprop_many(RmspropMany m, float 
 
 // ---------------------------------------------------------------- workspace
 
+// Library-owned workspace of the input gradients, one per device. It grows by allocating
+// a larger buffer; the old one is kept (never freed), so a graph that captured a call
+// keeps a valid pointer. hipMalloc is not allowed during capture: a capturing call that
+// would grow it is refused.
 std::mutex g_tw_mu;
 void *g_tw_ptr[64];
 size_t g_tw_bytes[64];
 
-hipError_t train_workspace(size_t bytes, void **out)
+hipError_t train_workspace(size_t bytes, hipStream_t s, void **out, const char **why)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -405,18 +409,21 @@ hipError_t train_workspace(size_t bytes, void **out)
     if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
     std::lock_guard<std::mutex> lk(g_tw_mu);
     if (g_tw_bytes[dev] < bytes) {
-        if (g_tw_ptr[dev]) {
-            e = hipFree(g_tw_ptr[dev]);
-            g_tw_ptr[dev] = nullptr;
-            g_tw_bytes[dev] = 0;
-            if (e != hipSuccess) return e;
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(s, &cs);
+        if (e != hipSuccess) return e;
+        if (cs != hipStreamCaptureStatusNone) {
+            *why = "the input-gradient workspace must grow and the stream is capturing (no "
+                   "allocation during capture): make one uncaptured call at the largest size first";
+            return hipErrorStreamCaptureUnsupported;
         }
-        const size_t want = bytes < ((size_t)16 << 20) ? ((size_t)16 << 20) : bytes;
-        e = hipMalloc(&g_tw_ptr[dev], want);
-        if (e != hipSuccess) {
-            g_tw_ptr[dev] = nullptr;
-            return e;
-        }
+        size_t want = 2 * g_tw_bytes[dev];
+        if (want < bytes) want = bytes;
+        if (want < ((size_t)16 << 20)) want = (size_t)16 << 20;
+        void *p = nullptr;
+        e = hipMalloc(&p, want);
+        if (e != hipSuccess) return e;
+        g_tw_ptr[dev] = p;          // the previous buffer stays allocated (see above)
         g_tw_bytes[dev] = want;
     }
     *out = g_tw_ptr[dev];
@@ -461,7 +468,7 @@ hipError_t launch_conv_input_grad(const uint16_t *grad_out, const uint16_t *w, c
     const size_t wbytes = ((size_t)fwd.cout * fwd.kh * fwd.kw * fwd.cin * 2 + 255) & ~(size_t)255;
     const size_t zbytes = fwd.stride == 2 ? (size_t)fwd.n * fwd.hin * fwd.win * fwd.cout * 2 : 0;
     void *ws = nullptr;
-    hipError_t e = train_workspace(wbytes + zbytes, &ws);
+    hipError_t e = train_workspace(wbytes + zbytes, s, &ws, why);
     if (e != hipSuccess) return e;
     uint16_t *wt = (uint16_t *)ws;
     const unsigned wblocks = blocks_for((long long)fwd.cout * fwd.kh * fwd.kw * fwd.cin);

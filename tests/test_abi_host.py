@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(B):
 
 
 def test_status_strings(B):
-    for s in range(11):
+    for s in range(12):
         assert B.status_name(s) and B.status_name(s) != "unknown status"
     assert B.status_name(99) == "unknown status"
 
