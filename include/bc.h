@@ -164,7 +164,7 @@ bc_status bc_scatter_blocks(const void *d_packed, const int32_t *d_idx, const in
  *    library, allocated by the first such call on the device and never freed or
  *    moved (a captured graph keeps a valid pointer whatever runs later). That first
  *    allocation is refused with BC_ERR_CAPTURE if the stream is capturing a graph:
- *    make one uncaptured call of such a layer first;
+ *    make one uncaptured call of such a layer first, or use bc_sparse_conv2d_noalloc;
  *  - per-tile arrival counters in a static device array; the last K slice of a tile
  *    resets its counter, so no clearing is needed between calls or graph replays.
  * Both are shared by every call on a device: calls on one device must not overlap
@@ -181,6 +181,31 @@ bc_status bc_sparse_conv2d(const bc_conv *conv,
                            void *d_out, bc_tensor out, bc_grid g,
                            const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
                            void *stream);
+
+/*
+ * bc_sparse_conv2d for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc. Same
+ * arguments, checks, kernels and results (bit for bit) as bc_sparse_conv2d; the only
+ * difference is where a layer that splits K keeps its fp32 partial tiles: in a fixed
+ * 16 MiB device array of the library (one per device, allocated when the library's
+ * code object is loaded on that device and held until the process ends), never in a
+ * workspace the call allocates. No call allocates or frees memory.
+ * The array holds the partials of any layer whose plan needs at most 16 MiB: every
+ * layer of ResNet-18/50 and SwiftNet at 2048x1024 with 128-pixel blocks. Layers whose
+ * partials need more (3x3 layers with 512 or more input channels and 513..2048 full-
+ * frame tiles of 64x64, e.g. 3x3 512->1024 on a 64x128 map with 8x8 blocks) are
+ * refused with BC_ERR_CAPACITY before anything is enqueued.
+ * The array and the split counters are shared by every call on a device and keep the
+ * last call's contents: calls on one device that overlap in time race (use one
+ * stream, or order streams with events). Nothing needs clearing between calls.
+ * Errors: those of bc_sparse_conv2d except BC_ERR_CAPTURE; BC_ERR_CAPACITY as above.
+ */
+bc_status bc_sparse_conv2d_noalloc(const bc_conv *conv,
+                                   const void *d_in, bc_tensor in,
+                                   const void *d_w, const float *d_bias, const void *d_residual,
+                                   void *d_out, bc_tensor out, bc_grid g,
+                                   const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                                   void *stream);
 
 /* The arguments of one bc_sparse_conv2d call (grid and index aside). */
 typedef struct bc_conv_call {

@@ -70,6 +70,8 @@ _sigs = {
     "bc_scatter_blocks": ([_vp, _vp, _vp, _i32, bc_grid, _vp, bc_tensor, _vp], _i32),
     "bc_sparse_conv2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, _vp, bc_tensor,
                           bc_grid, _vp, _vp, _i32, _vp], _i32),
+    "bc_sparse_conv2d_noalloc": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, _vp, _vp, _vp,
+                                  bc_tensor, bc_grid, _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_conv2d_pair": ([ctypes.POINTER(bc_conv_call), ctypes.POINTER(bc_conv_call), bc_grid,
                                _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_maxpool2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, bc_grid, _vp,
@@ -213,6 +215,15 @@ def bc_sparse_conv2d(conv, x, layout, w, bias, residual, out, grid, idx, count, 
                                _ptr(residual), _ptr(out), desc(out, layout), _grid(grid), _ptr(idx),
                                _ptr(count), cap, _stream(stream))
     _check(st, "bc_sparse_conv2d")
+
+
+def bc_sparse_conv2d_noalloc(conv, x, layout, w, bias, residual, out, grid, idx, count, stream=None):
+    cap = 0 if idx is None else int(idx.numel())
+    c = _conv(conv)
+    st = _lib.bc_sparse_conv2d_noalloc(ctypes.byref(c), _ptr(x), desc(x, layout), _ptr(w), _ptr(bias),
+                                       _ptr(residual), _ptr(out), desc(out, layout), _grid(grid),
+                                       _ptr(idx), _ptr(count), cap, _stream(stream))
+    _check(st, "bc_sparse_conv2d_noalloc")
 
 
 def _call(conv, x, layout, w, bias, residual, out) -> bc_conv_call:

@@ -376,12 +376,12 @@ bc_status conv_fail(hipError_t e, const char *why, const char *what)
 
 bc_status conv_launch(const bc_conv *conv, const void *d_in, const bc_tensor &in, const void *d_w,
                       const float *d_bias, const void *d_residual, void *d_out,
-                      const LayerGeom &L, hipStream_t s)
+                      const LayerGeom &L, hipStream_t s, bool noalloc = false)
 {
     const char *why = "";
     hipError_t e;
     if (in.layout == BC_NHWC) {
-        e = bc::launch_conv_nhwc_mfma((const uint16_t *)d_in, (const uint16_t *)d_w, d_bias,
+        e = (noalloc ? bc::launch_conv_nhwc_mfma_noalloc : bc::launch_conv_nhwc_mfma)((const uint16_t *)d_in, (const uint16_t *)d_w, d_bias,
                                       (const uint16_t *)d_residual, (uint16_t *)d_out, conv->relu,
                                       in.dtype == BC_BF16 ? bc::Half16::BF16 : bc::Half16::F16, L,
                                       s, &why);
@@ -416,6 +416,28 @@ bc_status bc_sparse_conv2d(const bc_conv *conv, const void *d_in, bc_tensor in, 
                                d_count, capacity, L);
     if (st) return st;
     if ((st = conv_launch(conv, d_in, in, d_w, d_bias, d_residual, d_out, L, (hipStream_t)stream)))
+        return st;
+    if (!d_idx) mark_full(d_out);
+    return ok();
+}
+
+bc_status bc_sparse_conv2d_noalloc(const bc_conv *conv, const void *d_in, bc_tensor in,
+                                   const void *d_w, const float *d_bias, const void *d_residual,
+                                   void *d_out, bc_tensor out, bc_grid g, const int32_t *d_idx,
+                                   const int32_t *d_count, int32_t capacity, void *stream)
+{
+    LayerGeom L;
+    bc_status st = conv_checks(conv, d_in, in, d_w, d_bias, d_residual, d_out, out, g, d_idx,
+                               d_count, capacity, L);
+    if (st) return st;
+    if (in.layout == BC_NHWC) {
+        const size_t need = bc::conv_nhwc_split_bytes(L), have = bc::conv_nhwc_scratch_bytes();
+        if (need > have)
+            return fail(BC_ERR_CAPACITY, "this layer's split-K partials need %zu bytes; the fixed "
+                                         "scratch array holds %zu (use bc_sparse_conv2d)", need, have);
+    }
+    if ((st = conv_launch(conv, d_in, in, d_w, d_bias, d_residual, d_out, L, (hipStream_t)stream,
+                          true)))
         return st;
     if (!d_idx) mark_full(d_out);
     return ok();

@@ -44,6 +44,15 @@ hipError_t launch_conv_nchw_f32(const float *x, const float *w, const float *bia
 hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const float *bias,
                                  const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
                                  const LayerGeom &g, hipStream_t s, const char **why);
+// The same layer with split-K partials in the library's fixed `scratch` array instead of
+// the allocated workspace: no allocation at any call. conv_nhwc_split_bytes gives the
+// partials' size of a layer's plan (0 if it does not split K), conv_nhwc_scratch_bytes
+// the array's size.
+hipError_t launch_conv_nhwc_mfma_noalloc(const uint16_t *x, const uint16_t *w, const float *bias,
+                                         const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
+                                         const LayerGeom &g, hipStream_t s, const char **why);
+size_t conv_nhwc_split_bytes(const LayerGeom &g);
+size_t conv_nhwc_scratch_bytes();
 // Two independent channels-last layers: one launch when both are 1x1 layers whose plans
 // pair (the second at stride 1, neither splitting K, BF16), else one launch each.
 struct ConvCall {

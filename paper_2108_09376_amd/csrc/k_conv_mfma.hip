@@ -1271,7 +1271,7 @@ constexpr size_t kWorkspaceBytes = (size_t)64 << 20;
 // the first call that splits K and never freed or moved, so a graph that captured a
 // split call keeps a valid pointer whatever runs later. hipMalloc is not allowed while
 // the stream is capturing: a capturing call that would allocate is refused (a prior
-// uncaptured split call on the device avoids that).
+// uncaptured split call on the device, or bc_sparse_conv2d_noalloc, avoids that).
 std::mutex g_ws_mu;
 void *g_ws_ptr[64];
 
@@ -1289,7 +1289,7 @@ hipError_t workspace(hipStream_t s, float **out, const char **why)
         if (cs != hipStreamCaptureStatusNone) {
             *why = "the split-K workspace of this device is not allocated yet and the stream is "
                    "capturing (no allocation during capture): make one uncaptured call that "
-                   "splits K first";
+                   "splits K first, or use bc_sparse_conv2d_noalloc";
             return hipErrorStreamCaptureUnsupported;
         }
         void *p = nullptr;
@@ -1298,6 +1298,33 @@ hipError_t workspace(hipStream_t s, float **out, const char **why)
         g_ws_ptr[dev] = p;
     }
     *out = (float *)g_ws_ptr[dev];
+    return hipSuccess;
+}
+
+// bc_sparse_conv2d_noalloc: the partials live in a fixed device array instead. In host
+// code `scratch` only names the symbol; its device address (one copy per device) comes
+// from hipGetSymbolAddress, taken once per device on the first call with that device
+// current, and only that address is passed to kernels.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+__device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+std::mutex g_scr_mu;
+float *g_scr_ptr[64];
+
+hipError_t scratch_ptr(float **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scr_mu);
+    if (!g_scr_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scr_ptr[dev] = (float *)p;
+    }
+    *out = g_scr_ptr[dev];
     return hipSuccess;
 }
 
@@ -1442,15 +1469,22 @@ void fill_plan(const uint16_t *x, const uint16_t *w, const float *bias, const ui
     a.f_bw = make_fastdiv(g.bw);
 }
 
-hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s, const char **why)
+// Where a split plan keeps its partials: the library-owned workspace, or the fixed
+// `scratch` array (bc_sparse_conv2d_noalloc).
+enum class Partials { Workspace, Scratch };
+
+hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s, const char **why,
+                       Partials where = Partials::Workspace)
 {
     if (p.grid == 0) return hipSuccess;
     if (p.ws_bytes) {
-        if (p.ws_bytes > kWorkspaceBytes) {
-            *why = "split-K partials larger than the workspace";
+        const size_t cap = where == Partials::Scratch ? kScratchBytes : kWorkspaceBytes;
+        if (p.ws_bytes > cap) {
+            *why = "split-K partials larger than the buffer that holds them";
             return hipErrorInvalidValue;
         }
-        const hipError_t e = workspace(s, &p.a.ws, why);
+        const hipError_t e = where == Partials::Scratch ? scratch_ptr(&p.a.ws)
+                                                        : workspace(s, &p.a.ws, why);
         if (e != hipSuccess) return e;
     }
     const hipError_t e = fmt == Half16::BF16 ? launch_geom<true>(p, g.kh, g.stride, s)
@@ -1493,6 +1527,24 @@ hipError_t launch_conv_nhwc_mfma(const uint16_t *x, const uint16_t *w, const flo
     Plan p;
     fill_plan(x, w, bias, res, y, relu, g, p);
     return launch_plan(p, fmt, g, s, why);
+}
+
+size_t conv_nhwc_split_bytes(const LayerGeom &g)
+{
+    Plan p;
+    return choose_plan(g, p) ? p.ws_bytes : 0;
+}
+
+size_t conv_nhwc_scratch_bytes() { return kScratchBytes; }
+
+hipError_t launch_conv_nhwc_mfma_noalloc(const uint16_t *x, const uint16_t *w, const float *bias,
+                                         const uint16_t *res, uint16_t *y, int relu, Half16 fmt,
+                                         const LayerGeom &g, hipStream_t s, const char **why)
+{
+    if (!conv_nhwc_mfma_supported(g, why)) return hipErrorInvalidValue;
+    Plan p;
+    fill_plan(x, w, bias, res, y, relu, g, p);
+    return launch_plan(p, fmt, g, s, why, Partials::Scratch);
 }
 
 hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Half16 fmt,

@@ -430,3 +430,63 @@ def test_runner_pairs_independent_layers_only():
     assert sorted((r50[i].name, r50[j].name) for i, j in found["r50"].items()) == [
         (f"layer{s}.0.downsample", f"layer{s}.0.conv1") for s in (1, 2, 3, 4)]
     assert not found["r18"]                    # its shortcuts pair with 3x3 layers only
+
+
+def noalloc_call(B, conv=(3, 3, 1, 1, 1), inp=(1, 64, 64, 128, 1, 1), out=(1, 64, 64, 128, 1, 1),
+                 grid=(8, 16), d_in=FAKE_IN, d_w=FAKE_W, d_out=FAKE_OUT, d_res=None,
+                 d_idx=FAKE_IDX, d_cnt=FAKE_CNT, cap=128):
+    lib = B.raw()
+    c = B.bc_conv(*conv)
+    st = lib.bc_sparse_conv2d_noalloc(ctypes.byref(c), d_in, B.bc_tensor(*inp), d_w, None, d_res,
+                                      d_out, B.bc_tensor(*out), B.bc_grid(*grid), d_idx, d_cnt, cap,
+                                      None)
+    return st, B.bc_last_error()
+
+
+@no_gpu
+def test_noalloc_validation_and_scratch_limit(B):
+    """bc_sparse_conv2d_noalloc checks its arguments as bc_sparse_conv2d does, then refuses
+    a layer whose split-K partials exceed the fixed 16 MiB scratch array with
+    BC_ERR_CAPACITY, before anything is enqueued (fake addresses)."""
+    E = B
+    assert noalloc_call(B, d_in=None)[0] == E.BC_ERR_NULL
+    assert noalloc_call(B, out=(1, 64, 32, 128, 1, 1))[0] == E.BC_ERR_SHAPE
+    assert noalloc_call(B, grid=(7, 16))[0] == E.BC_ERR_NOT_DIVISIBLE
+    assert noalloc_call(B, d_out=FAKE_IN + 100)[0] == E.BC_ERR_ALIAS
+    assert noalloc_call(B, out=(1, 48, 64, 128, 1, 1))[0] == E.BC_ERR_UNSUPPORTED
+    # 3x3 512 -> 1024 on a 64x128 map with 8x8 blocks: 2048 full-frame tiles split in two,
+    # 2048 * 2 * 64 * 64 * 4 bytes = 64 MiB of partials
+    st, msg = noalloc_call(B, inp=(1, 512, 64, 128, 1, 1), out=(1, 1024, 64, 128, 1, 1))
+    assert st == E.BC_ERR_CAPACITY and "scratch" in msg
+    # 3x3 1024 -> 512: 1024 tiles, 32 MiB
+    st, _ = noalloc_call(B, inp=(1, 1024, 64, 128, 1, 1), out=(1, 512, 64, 128, 1, 1))
+    assert st == E.BC_ERR_CAPACITY
+
+
+def _fits_scratch(B, layer, shape_in, grid):
+    """Status class of a noalloc call for one network layer on fake addresses: with no
+    GPU a call that passes every check fails at the launch (BC_ERR_HIP), one that
+    needs more scratch fails with BC_ERR_CAPACITY."""
+    ih, iw, cin = shape_in
+    k, s = layer.k, layer.stride
+    oh, ow = (ih + 2 * (k // 2) - k) // s + 1, (iw + 2 * (k // 2) - k) // s + 1
+    st, msg = noalloc_call(B, conv=(k, k, s, k // 2, 1), inp=(1, cin, ih, iw, 1, 1),
+                           out=(1, layer.cout, oh, ow, 1, 1), grid=grid)
+    return st, msg
+
+
+@no_gpu
+@pytest.mark.parametrize("net", ["resnet18", "resnet50", "swiftnet18", "swiftnet50"])
+def test_noalloc_scratch_holds_every_network_layer(B, net):
+    """Every convolution of the 2048x1024 networks with 128-pixel blocks fits the fixed
+    scratch array (the claim of include/bc.h)."""
+    from paper_2108_09376_amd import resnet
+    depth = int(net[-2:])
+    layers = (resnet.build_swiftnet_layers(depth) if net.startswith("swift")
+              else resnet.build_layers(depth))
+    shapes = resnet.layer_shapes(layers, 1024, 2048)
+    for l in layers:
+        if l.kind != "conv" or l.src < 0:
+            continue                       # the stem's input is the frame (3 channels)
+        st, msg = _fits_scratch(B, l, shapes[l.src], (8, 16))
+        assert st != B.BC_ERR_CAPACITY, (net, l.name, msg)
