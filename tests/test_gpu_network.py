@@ -231,6 +231,10 @@ FULL = [
     (512, 512, 32, 64, 8, 16, 3, 1, False),      # stride-32 3x3: K split over two workgroups
     (2048, 512, 32, 64, 8, 16, 1, 1, False),     # stride-32 1x1: K split over three workgroups
 ]
+# the rest of the stride-16 sweep: every (Cin, Cout) in {256, 512, 1024}^2, 1x1 and 3x3
+FULL += [(ci, co, 64, 128, 8, 16, k, 1, k == 1 and co > ci)
+         for k in (1, 3) for ci in (256, 512, 1024) for co in (256, 512, 1024)
+         if not any(c[0] == ci and c[1] == co and c[2] == 64 and c[6] == k and c[7] == 1 for c in FULL)]
 
 
 @pytest.mark.parametrize("case", FULL, ids=[f"c{c[0]}-{c[1]}_k{c[6]}s{c[7]}_{c[2]}x{c[3]}" for c in FULL])
