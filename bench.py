@@ -57,6 +57,12 @@ def parse():
                     help="skip the single-layer shapes (256x512x64 3x3; stride-16 C sweep)")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="run only N plain steps (for rocprofv3) and print nothing else")
+    ap.add_argument("--counter-summary", nargs=2, metavar=("COUNTER_CSV", "AGENT_CSV"),
+                    help="print the matrix-core / LDS counter table of a rocprofv3 --pmc run")
+    ap.add_argument("--pmc-gather-scatter", action="store_true",
+                    help="run only the standalone gather/scatter cases for a rocprofv3 --pmc run")
+    ap.add_argument("--gs-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the gather/scatter traffic table of two rocprofv3 --pmc runs")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the HBM-traffic summary of two counter_collection.csv files and exit")
     ap.add_argument("--rocprof-summary", nargs="+", metavar="CSV",
@@ -336,8 +342,119 @@ def gather_scatter(torch, bc, dev):
                                    "cold_us": round(cold_us, 2),
                                    "cold_GBps": round(nbytes / cold_us / 1e3, 1),
                                    "cold_frac_of_hbm_peak": round(nbytes / cold_us / 1e3 / PEAK_HBM_GBS, 3)}
+            hb = (recorded_gs_bytes() or {}).get(f"{name}_C{c}")
+            if hb is not None:
+                # HBM bytes the counters saw for one cold launch, over the same cold time
+                out[f"{name}_C{c}"].update({"counter_bytes": round(hb), "counter_GBps_cold": round(hb / cold_us / 1e3, 1),
+                                            "counter_frac_of_hbm_peak": round(hb / cold_us / 1e3 / PEAK_HBM_GBS, 3)})
             del g
     return out
+
+
+GS_CASES = (("C64", 64, False), ("C256", 256, False), ("all_blocks_C256", 256, True))
+GS_PROFILE = os.path.join(ROOT, "profiles", "gather_scatter_traffic_256x512_bf16.txt")
+GS_SOURCES = ("paper_2108_09376_amd/csrc/k_gather_scatter.hip",)
+
+
+def gs_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GS_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def gs_algo_bytes(c, all_blocks, n_act=38):
+    n = 128 if all_blocks else n_act
+    return {"gather": 2 * n * 34 * 34 * c * 2, "scatter": 2 * n * 32 * 32 * c * 2}
+
+
+def pmc_gather_scatter(torch, bc, dev, reps=3):
+    """Counter runs of the standalone gather and scatter (rocprofv3 --pmc FETCH_SIZE,
+    then WRITE_SIZE): the calibration negation (256 MiB read, 256 MiB written), then
+    `reps` rounds of gather / scatter on the tensors of gather_scatter() for C = 64,
+    C = 256 and C = 256 with every block, each op after a 512 MiB cache-evicting read."""
+    import synth
+    mask = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
+    m = torch.from_numpy(mask).to(dev)
+    idx = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+    bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
+    idx_all = torch.arange(128, dtype=torch.int32, device=dev)
+    cnt_all = torch.full((1,), 128, dtype=torch.int32, device=dev)
+    a0 = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+    a1 = torch.empty_like(a0)
+    torch.cuda.synchronize()
+    torch.neg(a0, out=a1)
+    torch.cuda.synchronize()
+    del a0, a1
+    flush = torch.ones((4096, 32768), dtype=torch.float32, device=dev)
+    flush_out = torch.empty(4096, dtype=torch.float32, device=dev)
+    tens = {}
+    for c in (64, 256):
+        tens[c] = (torch.randn((1, 256, 512, c), device=dev).to(torch.bfloat16),
+                   torch.empty((128, 34, 34, c), dtype=torch.bfloat16, device=dev),
+                   torch.randn((128, 32, 32, c), device=dev).to(torch.bfloat16),
+                   torch.empty((1, 256, 512, c), dtype=torch.bfloat16, device=dev))
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        for _, c, allb in GS_CASES:
+            x, packed, blocks, dst = tens[c]
+            i, n = (idx_all, cnt_all) if allb else (idx, cnt)
+            torch.amax(flush, dim=1, out=flush_out)
+            bc.bc_gather_halo(x, bc.BC_NHWC, (8, 16), (3, 3, 1, 1, 0), 0.0, i, n, packed)
+            torch.amax(flush, dim=1, out=flush_out)
+            bc.bc_scatter_blocks(blocks, i, n, (8, 16), dst, bc.BC_NHWC)
+    torch.cuda.synchronize()
+
+
+def gs_summary(fetch_csv, write_csv):
+    """Text summary of the two counter runs of pmc_gather_scatter: calibrated FETCH and
+    WRITE bytes per gather / scatter dispatch against the algorithmic bytes."""
+    import csv
+    res = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = int(r["Dispatch_Id"])
+            rows[d] = (r["Kernel_Name"], rows.get(d, (None, 0.0))[1] + float(r["Counter_Value"]))
+        seq = [rows[d] for d in sorted(rows)]
+        cal = [v for n, v in seq if "neg" in n.lower()]
+        factor = (256 << 10) / cal[-1]
+        ops = [v * factor * 1024 for n, v in seq if "k_gather_" in n or "k_scatter_" in n]
+        if len(ops) % 6:
+            raise SystemExit(f"{path}: {len(ops)} gather/scatter dispatches is not a whole number of rounds")
+        res[counter] = (factor, [ops[i:i + 6] for i in range(0, len(ops), 6)])
+    out = [f"calibration factors: FETCH_SIZE {res['FETCH_SIZE'][0]:.4f}, WRITE_SIZE {res['WRITE_SIZE'][0]:.4f}",
+           f"{'op':26s} {'fetch_MB':>9s} {'write_MB':>9s} {'hbm_MB':>9s} {'algo_MB':>9s} {'ratio':>6s}"]
+    kv = []
+    for k, (tag, c, allb) in enumerate(GS_CASES):
+        algo = gs_algo_bytes(c, allb)
+        for j, op in enumerate(("gather", "scatter")):
+            col = 2 * k + j
+            f = sum(r[col] for r in res["FETCH_SIZE"][1]) / len(res["FETCH_SIZE"][1])
+            w = sum(r[col] for r in res["WRITE_SIZE"][1]) / len(res["WRITE_SIZE"][1])
+            out.append(f"{op + '_' + tag:26s} {f / 1e6:9.3f} {w / 1e6:9.3f} {(f + w) / 1e6:9.3f} "
+                       f"{algo[op] / 1e6:9.3f} {(f + w) / algo[op]:6.2f}")
+            kv.append(f"hbm_bytes_{op}_{tag}={f + w:.0f}")
+    out += kv
+    out.append(f"gs_source_sha256={gs_source_sha()}")
+    return "\n".join(out)
+
+
+def recorded_gs_bytes():
+    """Counter HBM bytes per gather / scatter case from the committed summary (None if
+    missing or taken on other kernel sources)."""
+    try:
+        kv = dict(l.split("=", 1) for l in open(GS_PROFILE).read().splitlines() if "=" in l
+                  and " " not in l.split("=", 1)[0])
+    except OSError:
+        return None
+    if kv.get("gs_source_sha256") != gs_source_sha():
+        return None
+    return {k[len("hbm_bytes_"):]: float(v) for k, v in kv.items() if k.startswith("hbm_bytes_")}
 
 
 def policy_steps(torch, bc, dev):
@@ -594,6 +711,7 @@ def swiftnet_clip_step(torch, bc, dev, frames=30, seed=2021):
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "sparse_conv_traffic_resnet50_2048x1024_active0.3.txt")
+MFMA_PROFILE = os.path.join(ROOT, "profiles", "sparse_conv_mfma_lds_resnet50_2048x1024_active0.3.txt")
 CONV_SOURCES = ("paper_2108_09376_amd/csrc/k_conv_mfma.hip", "paper_2108_09376_amd/csrc/bc_internal.h")
 
 
@@ -667,6 +785,75 @@ def pmc_summary(fetch_csv, write_csv):
     return "\n".join(out)
 
 
+def counter_summary(counter_csv, agent_csv):
+    """Text summary of a rocprofv3 --pmc run of `bench.py --pmc-frames N` with the
+    matrix-core and LDS counters (MfmaUtil LdsUtil LdsBankConflict
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_LDS SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE
+    SQ_BUSY_CYCLES). Per conv layer, mean over the sparse frames: the kernel's duration;
+    mfma_util = MFMA busy cycles summed over every SIMD / (SIMDs x duration x peak
+    engine clock), the counters' utilisation over the kernel's own run time; rocprof's
+    MfmaUtil / LdsUtil / LdsBankConflict (percent of GRBM_GUI_ACTIVE, a window that
+    also holds the profiler's per-dispatch set-up, so they read lower); and the
+    matrix-core FLOPs the counters saw (MOPS x 512) over the algorithmic FLOPs."""
+    import csv
+
+    from paper_2108_09376_amd import resnet
+    agent = [r for r in csv.DictReader(open(agent_csv)) if r.get("Name", "").startswith("gfx")][0]
+    simds, clk = int(agent["Simd_Count"]), float(agent["Max_Engine_Clk_Fcompute"]) * 1e6
+    per = {}
+    for r in csv.DictReader(open(counter_csv)):
+        d = per.setdefault(int(r["Dispatch_Id"]), {
+            "name": r["Kernel_Name"],
+            "dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    conv = [per[k] for k in sorted(per) if "k_conv_" in per[k]["name"]]
+    if len(conv) % 53:
+        raise SystemExit(f"{counter_csv}: {len(conv)} conv dispatches is not a whole number of frames")
+    frames = [conv[i:i + 53] for i in range(0, len(conv), 53)][1:]
+    layers = resnet.build_layers(50)
+    shapes = resnet.layer_shapes(layers, 1024, 2048)
+    flops = [2.0 * l.cin * l.cout * l.k * l.k * oh * ow * 38 / 128
+             for l, (oh, ow, _) in zip(layers, shapes) if l.kind == "conv"]
+    names = [l.name for l in layers if l.kind == "conv"]
+
+    def mean(i, key):
+        return sum(f[i][key] for f in frames) / len(frames)
+
+    out = [f"device: {simds} SIMDs, peak engine clock {clk / 1e9:.2f} GHz; one 16x16x32 bf16 MFMA "
+           f"holds a SIMD's matrix core for 16 cycles, so busy cycles x 16384 / 16 = FLOPs at peak",
+           f"{'layer':24s} {'us':>7s} {'mfma_util':>9s} {'MfmaUtil%':>9s} {'LdsUtil%':>8s} "
+           f"{'LdsBank%':>8s} {'flop/algo':>9s}"]
+    tb = td = 0.0
+    for i in range(53):
+        busy, dur = mean(i, "SQ_VALU_MFMA_BUSY_CYCLES"), mean(i, "dur")
+        tb += busy
+        td += dur
+        out.append(f"{names[i]:24s} {dur * 1e6:7.2f} {busy / (simds * dur * clk):9.4f} "
+                   f"{mean(i, 'MfmaUtil'):9.2f} {mean(i, 'LdsUtil'):8.2f} {mean(i, 'LdsBankConflict'):8.3f} "
+                   f"{mean(i, 'SQ_INSTS_VALU_MFMA_MOPS_BF16') * 512 / flops[i]:9.3f}")
+    out.append(f"sparse frame (38/128 blocks), mean of {len(frames)} frames: {td * 1e6:.1f} us of conv "
+               f"kernels under the profiler (kernels serialised, counters set up per dispatch), MFMA "
+               f"busy {tb / simds / clk * 1e6:.2f} us per SIMD; the algorithmic {sum(flops) / 1e9:.1f} GFLOP "
+               f"take {sum(flops) / (simds * clk * 16384 / 16) * 1e6:.2f} us per SIMD at peak")
+    out.append(f"mfma_util_over_conv_kernel_time={tb / (simds * td * clk):.4f}")
+    out.append(f"mfma_busy_us_per_simd_per_frame={tb / simds / clk * 1e6:.3f}")
+    out.append(f"conv_source_sha256={conv_source_sha()}")
+    return "\n".join(out)
+
+
+def recorded_mfma_busy_us():
+    """Matrix-core busy time per SIMD of one sparse frame's convolutions (counters), from
+    the committed summary, or None if it is missing or was taken on other kernel sources."""
+    try:
+        kv = dict(l.split("=", 1) for l in open(MFMA_PROFILE).read().splitlines() if "=" in l
+                  and " " not in l.split("=", 1)[0])
+    except OSError:
+        return None
+    if kv.get("conv_source_sha256") != conv_source_sha():
+        return None
+    return float(kv["mfma_busy_us_per_simd_per_frame"])
+
+
 def recorded_traffic():
     """HBM bytes per sparse-conv launch from the committed counter summary, or None if
     it is missing or was taken on other kernel sources."""
@@ -722,6 +909,12 @@ def main():
     if args.pmc_summary:
         print(pmc_summary(*args.pmc_summary))
         return
+    if args.counter_summary:
+        print(counter_summary(*args.counter_summary))
+        return
+    if args.gs_summary:
+        print(gs_summary(*args.gs_summary))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
@@ -733,6 +926,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.pmc_gather_scatter:
+        from paper_2108_09376_amd import bc
+        pmc_gather_scatter(torch, bc, dev)
+        return
     H, W, BLOCK = 1024, 2048, 128
     net = resnet.SparseResNet(50, H, W, BLOCK, device=dev)
     # counter runs take one dispatch per conv layer (the per-layer traffic table)
@@ -902,6 +1099,8 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "avg_launch_us": round(per_launch_us, 3), "conv_us_per_frame": round(conv_total_us, 2),
                      "traffic": recorded_traffic(),
+                     "mfma_util": (None if recorded_mfma_busy_us() is None else
+                                   round(recorded_mfma_busy_us() / conv_total_us, 4)),
                      "algo_bytes_per_launch": round(sum(b for b in resnet.conv_algo_bytes(
                          net.layers, net.shapes, net.grid, active) if b) / len(conv_idx)),
                      "trace_conv_dispatch_window": conv_window,
