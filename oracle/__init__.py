@@ -273,6 +273,92 @@ def sparse_upsample_add(coarse_bits, skip_bits, mask, prev_bits, dtype, relu=Fal
     return select(mask, fresh, prev_bits, z.shape[2] // gh, z.shape[3] // gw)
 
 
+# ------------------------------------------------------------------ pyramid pooling
+#
+# The segmentation network's context module on the encoder's stride-32 output (the
+# spatial pyramid pooling of SwiftNet-style models; the paper makes every layer of such
+# single-stage networks block-sparse, Section 4). Each pyramid level averages the whole
+# map over a grid of bins, so a level depends on every block of its input: under the
+# method's dense-then-select definition the levels are computed densely from the
+# layer's current input buffer each frame (fresh where blocks ran, transferred
+# elsewhere), and only the concatenated output is selected into the previous output.
+
+def spp_bins(h, w, g):
+    """Bin grid of a pyramid level with g rows on an h x w map: g rows (at most h) and
+    g * w / h columns rounded to the nearest integer (at least 1, at most w), so bins
+    stay about square on maps wider than tall."""
+    rows = min(g, h)
+    cols = min(w, max(1, int(np.floor(g * w / h + 0.5))))
+    return rows, cols
+
+
+def adaptive_avg_pool2d(x, oh, ow):
+    """Mean of each of oh x ow bins of [n, c, h, w] values (float64): bin (i, j) covers
+    rows floor(i h / oh) .. ceil((i + 1) h / oh) - 1 and the same for columns."""
+    x = np.asarray(x, np.float64)
+    n, c, h, w = x.shape
+    out = np.empty((n, c, oh, ow), np.float64)
+    for i in range(oh):
+        r0, r1 = (i * h) // oh, -((-(i + 1) * h) // oh)
+        for j in range(ow):
+            c0, c1 = (j * w) // ow, -((-(j + 1) * w) // ow)
+            out[:, :, i, j] = x[:, :, r0:r1, c0:c1].mean(axis=(2, 3))
+    return out
+
+
+def upsample_bilinear(x, oh, ow):
+    """Bilinear resampling of [n, c, h, w] values (float64) to oh x ow with pixel centres
+    aligned: output row Y samples input row s = (Y + 1/2) h / oh - 1/2, taken as 0 when
+    negative; with i0 = floor(s), i1 = min(i0 + 1, h - 1) and f = s - i0 it is
+    (1 - f) x[i0] + f x[i1]. The same along columns."""
+    x = np.asarray(x, np.float64)
+
+    def axis_resample(a, axis, n_out):
+        n_in = a.shape[axis]
+        src = np.maximum((np.arange(n_out) + 0.5) * (n_in / n_out) - 0.5, 0.0)
+        i0 = np.floor(src).astype(np.int64)
+        i0 = np.minimum(i0, n_in - 1)
+        i1 = np.minimum(i0 + 1, n_in - 1)
+        f = src - i0
+        shape = [1] * a.ndim
+        shape[axis] = n_out
+        f = f.reshape(shape)
+        return np.take(a, i0, axis=axis) * (1.0 - f) + np.take(a, i1, axis=axis) * f
+
+    return axis_resample(axis_resample(x, 2, oh), 3, ow)
+
+
+def spp_levels(b_bits, grid_rows, w_bits, bias, dtype):
+    """The pyramid levels of the bottleneck map b ([n, c, h, w] bit patterns), every
+    pixel: per level l with grid_rows[l] rows, the bins' means (spp_bins), a 1x1
+    convolution with weights w_bits[l] ([cl, c] bit patterns) plus bias[l] (fp32
+    values), ReLU, rounded to dtype. Returns a list of [n, cl, rows, cols] bit patterns."""
+    b = value(b_bits, dtype)
+    n, c, h, w = b.shape
+    out = []
+    for g, wl, bl in zip(grid_rows, w_bits, bias):
+        rows, cols = spp_bins(h, w, g)
+        pooled = adaptive_avg_pool2d(b, rows, cols)
+        wv = value(wl, dtype).reshape(wl.shape[0], c)
+        z = np.einsum("oc,nchw->nohw", wv, pooled) + np.asarray(bl, np.float32).astype(np.float64)[None, :, None, None]
+        out.append(store(np.maximum(z, 0.0), dtype))
+    return out
+
+
+def sparse_spp(b_bits, level_bits, mask, prev_bits, dtype):
+    """The pyramid pooling's concatenated output, block-sparse: channels 0..c-1 are the
+    bottleneck map itself (its stored bits), then each level upsampled bilinearly to the
+    map's size (upsample_bilinear) and rounded to dtype; executed blocks take these
+    values, every other element keeps prev_bits."""
+    n, c, h, w = b_bits.shape
+    parts = [b_bits]
+    for lb in level_bits:
+        parts.append(store(upsample_bilinear(value(lb, dtype), h, w), dtype))
+    fresh = np.concatenate(parts, axis=1)
+    gh, gw = np.asarray(mask).shape[1:]
+    return select(mask, fresh, prev_bits, h // gh, w // gw)
+
+
 def gather_halo(x_bits, idx, gh, gw, bh, bw, kh, kw, stride, pad, pad_bits):
     """Halo tiles of the listed output blocks, packed [K, th, tw, C] (channels last):
     packed[k, i, j, c] = X[n, c, gy*bh*s - pad + i, gx*bw*s - pad + j], with

@@ -19,7 +19,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import fold_bn, sparse_conv2d, sparse_maxpool2d, sparse_upsample_add, store
+from . import (fold_bn, sparse_conv2d, sparse_maxpool2d, sparse_spp, sparse_upsample_add, spp_levels,
+               store)
 
 
 def resnet_table(depth: int):
@@ -64,17 +65,23 @@ def resnet_table(depth: int):
     return L
 
 
+SPP_GRID = (8, 4, 2, 1)      # rows of the pyramid levels' bin grids
+
+
 def swiftnet_table(depth: int = 18, classes: int = 19, width: int = 128):
     """A SwiftNet-like single-scale segmentation network (Orsic et al., 2019; the
-    paper's semantic segmentation model, Section 4): the ResNet encoder above, then a
-    decoder that runs at strides 32 -> 16 -> 8 -> 4. Each merge upsamples the coarser
-    decoder feature by two (bilinear) and adds a 1x1 lateral projection of the encoder
-    feature of the finer stride, then blends with a 3x3 convolution; a 1x1 head gives
-    the class scores at stride 4. Reading: the pyramid pooling on the stride-32
-    feature pools over the whole image, not per block, and is replaced by a 1x1
-    projection; the head computes a multiple of 64 channels (what the matrix-core
-    layers take) of which the first `classes` are the class scores. New layer kind
-    'up': src = coarse feature, res = lateral (skip)."""
+    paper's semantic segmentation model, Section 4, with a ResNet backbone): the ResNet
+    encoder above, a spatial pyramid pooling module on the stride-32 feature, then a
+    decoder that runs at strides 32 -> 16 -> 8 -> 4. Pyramid pooling: a 1x1 bottleneck
+    to `width` channels; levels with 8, 4, 2 and 1 rows of bins (spp_bins), each the
+    bins' means, a 1x1 convolution to width/4 channels and ReLU, upsampled bilinearly
+    to the map and concatenated after the bottleneck (kind 'spp', computed densely and
+    selected, see oracle.sparse_spp); a 1x1 fuse back to `width`. Each merge upsamples
+    the coarser decoder feature by two (bilinear) and adds a 1x1 lateral projection of
+    the encoder feature of the finer stride, then blends with a 3x3 convolution; a 1x1
+    head gives the class scores at stride 4. Reading: the head computes a multiple of 64
+    channels (what the matrix-core layers take) of which the first `classes` are the
+    class scores. Layer kind 'up': src = coarse feature, res = lateral (skip)."""
     L = resnet_table(depth)
     ends = {}
     for i, l in enumerate(L):
@@ -87,7 +94,12 @@ def swiftnet_table(depth: int = 18, classes: int = 19, width: int = 128):
                       k=k, stride=1, pad=k // 2, relu=relu))
         return len(L) - 1
 
-    x = conv("dec.proj4", ends[4], 512 * expansion, width, 1, True)
+    b = conv("dec.spp.bottleneck", ends[4], 512 * expansion, width, 1, True)
+    cl = width // 4
+    cat = width + len(SPP_GRID) * cl
+    L.append(dict(kind="spp", name="dec.spp", src=b, res=None, cin=width, cout=cat, k=1, stride=1,
+                  pad=0, relu=True, grid=SPP_GRID, cl=cl))
+    x = conv("dec.spp.fuse", len(L) - 1, cat, width, 1, True)
     for s in (3, 2, 1):
         lat = conv(f"dec.lat{s}", ends[s], (64 << (s - 1)) * expansion, width, 1, True)
         L.append(dict(kind="up", name=f"dec.up{s}", src=x, res=lat, cin=width, cout=width,
@@ -145,35 +157,47 @@ def dense_frame(table, folded, x_bits, dtype):
 
 def make_params(table, seed0=1000, bn_random=False):
     """Per-conv fp32 OIHW weights (He-normal, seed seed0 + layer index) and BN
-    parameters. Random init uses gamma=1, beta=0, mean=0, var=1 unless bn_random."""
+    parameters; a pyramid pooling layer gets one such set per level (1x1, cl x cin),
+    drawn in level order from the layer's seed. Random init uses gamma=1, beta=0,
+    mean=0, var=1 unless bn_random."""
     import synth
     params = []
-    for li, l in enumerate(table):
-        if l["kind"] != "conv":
-            params.append(None)
-            continue
-        r = synth.rng(seed0 + li)
-        w = synth.he_normal(r, l["cout"], l["cin"], l["k"], l["k"])
-        c = l["cout"]
+
+    def one(r, cout, cin, k):
+        w = synth.he_normal(r, cout, cin, k, k)
         if bn_random:
-            bn = dict(gamma=r.uniform(0.5, 1.5, c), beta=r.normal(0, 0.1, c),
-                      mean=r.normal(0, 0.1, c), var=r.uniform(0.5, 1.5, c))
+            bn = dict(gamma=r.uniform(0.5, 1.5, cout), beta=r.normal(0, 0.1, cout),
+                      mean=r.normal(0, 0.1, cout), var=r.uniform(0.5, 1.5, cout))
         else:
-            bn = dict(gamma=np.ones(c), beta=np.zeros(c), mean=np.zeros(c), var=np.ones(c))
-        params.append(dict(w=w, **bn))
+            bn = dict(gamma=np.ones(cout), beta=np.zeros(cout), mean=np.zeros(cout), var=np.ones(cout))
+        return dict(w=w, **bn)
+
+    for li, l in enumerate(table):
+        r = synth.rng(seed0 + li)
+        if l["kind"] == "conv":
+            params.append(one(r, l["cout"], l["cin"], l["k"]))
+        elif l["kind"] == "spp":
+            params.append(dict(levels=[one(r, l["cl"], l["cin"], 1) for _ in l["grid"]]))
+        else:
+            params.append(None)
     return params
 
 
 def fold_params(table, params, dtype):
     """BN folded in fp64; weights rounded to the storage dtype (bit patterns),
-    bias rounded to fp32."""
+    bias rounded to fp32 (per level for a pyramid pooling layer)."""
+    def one(p):
+        w2, b2 = fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
+        return dict(w_bits=store(w2, dtype), bias=b2.astype(np.float32))
+
     out = []
     for l, p in zip(table, params):
         if p is None:
             out.append(None)
-            continue
-        w2, b2 = fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
-        out.append(dict(w_bits=store(w2, dtype), bias=b2.astype(np.float32)))
+        elif l["kind"] == "spp":
+            out.append(dict(levels=[one(q) for q in p["levels"]]))
+        else:
+            out.append(one(p))
     return out
 
 
@@ -204,6 +228,10 @@ def frame(table, folded, x_bits, mask, prev, dtype):
             y = sparse_maxpool2d(src, mask, prev[li], dtype, l["k"], l["stride"], l["pad"])
         elif l["kind"] == "up":
             y = sparse_upsample_add(src, bufs[l["res"]], mask, prev[li], dtype, relu=l["relu"])
+        elif l["kind"] == "spp":
+            lv = folded[li]["levels"]
+            levels = spp_levels(src, l["grid"], [q["w_bits"] for q in lv], [q["bias"] for q in lv], dtype)
+            y = sparse_spp(src, levels, mask, prev[li], dtype)
         else:
             res = None if l["res"] is None else bufs[l["res"]]
             y = sparse_conv2d(src, folded[li]["w_bits"], mask, prev[li], dtype,
