@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BC_ABI_VERSION 9
+#define BC_ABI_VERSION 10
 
 typedef enum {
     BC_OK = 0,
@@ -236,6 +236,43 @@ typedef struct bc_conv_call {
 bc_status bc_sparse_conv2d_pair(const bc_conv_call *a, const bc_conv_call *b, bc_grid g,
                                 const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
                                 void *stream);
+
+/* Pyramid pooling geometry: `levels` levels (1..8); level l averages the input over a
+ * rows[l] x cols[l] grid of bins (1 <= rows[l] <= h, 1 <= cols[l] <= w) and projects to
+ * cl channels (cl % 8 == 0, 8 <= cl <= 256). */
+typedef struct { int32_t levels, cl; int32_t rows[8], cols[8]; } bc_spp_geom;
+
+/*
+ * Block-sparse spatial pyramid pooling: the context module of SwiftNet-style
+ * segmentation networks on the encoder's last feature, run like every other layer of
+ * a single-stage network (Section 4), with the layer result defined as the dense
+ * layer on the current input buffer selected into the previous output (Section 3.1):
+ *   level l (every pixel, every call): bin (i, j) of the rows[l] x cols[l] grid covers
+ *     input rows floor(i h / rows) .. ceil((i+1) h / rows) - 1 (same for columns);
+ *     L_l[i][j] = round(ReLU(bias[l] + W[l] . mean of the bin)), W[l] a 1x1 conv
+ *     [cl][c], written to d_levels [n][bins][cl] (bins = sum of rows[l] * cols[l],
+ *     level by level, raster order);
+ *   out[block] = [in, up(L_0), ..., up(L_{levels-1})] on the active blocks, where up()
+ *     resamples to h x w bilinearly with pixel centres aligned (output row y samples
+ *     level row ((2y + 1) rows - h) / (2h), 0 if negative, neighbours clamped) and
+ *     rounds once; out[other] untouched (feature transfer).
+ * Because the levels pool the whole map, they read every block of d_in (fresh where
+ * blocks ran this frame, transferred elsewhere); the concatenation is written at the
+ * active blocks only. Arithmetic in fp32 (sums in a fixed order), RNE to the dtype.
+ *   in        NHWC BF16/F16 [n][h][w][c], c % 8 == 0 and c / 8 dividing 256 (c <= 2048).
+ *   d_w       [levels][cl][c] in in.dtype (batch norm folded, bc_fold_bn).
+ *   d_bias    [levels][cl] fp32, or NULL.
+ *   d_levels  caller-owned scratch [n][bins][cl] in in.dtype, rewritten by every call.
+ *   out       [n][h][w][c + levels * cl], same dtype and layout; grid blocks of out.
+ * Registered-buffer rule as bc_sparse_conv2d. Errors: BC_ERR_NULL, BC_ERR_SHAPE,
+ * BC_ERR_DTYPE, BC_ERR_LAYOUT, BC_ERR_NOT_DIVISIBLE, BC_ERR_CAPACITY, BC_ERR_ALIAS,
+ * BC_ERR_UNINITIALIZED, BC_ERR_UNSUPPORTED, BC_ERR_HIP.
+ */
+bc_status bc_sparse_spp(const void *d_in, bc_tensor in, const bc_spp_geom *spp,
+                        const void *d_w, const float *d_bias, void *d_levels,
+                        void *d_out, bc_tensor out, bc_grid g,
+                        const int32_t *d_idx, const int32_t *d_count, int32_t capacity,
+                        void *stream);
 
 /*
  * Block-sparse max pooling (the ResNet stem pooling run block-sparsely), kernel

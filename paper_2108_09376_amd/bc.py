@@ -48,6 +48,11 @@ class bc_conv(ctypes.Structure):
                 ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
 
 
+class bc_spp_geom(ctypes.Structure):
+    _fields_ = [("levels", ctypes.c_int32), ("cl", ctypes.c_int32), ("rows", ctypes.c_int32 * 8),
+                ("cols", ctypes.c_int32 * 8)]
+
+
 class bc_conv_call(ctypes.Structure):
     _fields_ = [("conv", bc_conv), ("d_in", ctypes.c_void_p), ("in_", bc_tensor),
                 ("d_w", ctypes.c_void_p), ("d_bias", ctypes.c_void_p),
@@ -74,6 +79,8 @@ _sigs = {
                                   bc_tensor, bc_grid, _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_conv2d_pair": ([ctypes.POINTER(bc_conv_call), ctypes.POINTER(bc_conv_call), bc_grid,
                                _vp, _vp, _i32, _vp], _i32),
+    "bc_sparse_spp": ([_vp, bc_tensor, ctypes.POINTER(bc_spp_geom), _vp, _vp, _vp, _vp, bc_tensor, bc_grid,
+                       _vp, _vp, _i32, _vp], _i32),
     "bc_sparse_maxpool2d": ([ctypes.POINTER(bc_conv), _vp, bc_tensor, _vp, bc_tensor, bc_grid, _vp,
                              _vp, _i32, _vp], _i32),
     "bc_fold_bn": ([_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp], _i32),
@@ -108,7 +115,7 @@ EXPORTED = tuple(_sigs)
 
 # The ABI these bindings marshal for (BC_ABI_VERSION of include/bc.h); a library built
 # from other sources is refused rather than called with mismatched arguments.
-ABI_VERSION = 9
+ABI_VERSION = 10
 if _lib.bc_abi_version() != ABI_VERSION:
     raise ImportError(f"{LIB_PATH} has ABI {_lib.bc_abi_version()}, the bindings expect "
                       f"{ABI_VERSION}: rebuild with `python -m paper_2108_09376_amd.build`")
@@ -241,6 +248,19 @@ def bc_sparse_conv2d_pair(a, b, grid, idx, count, stream=None):
     st = _lib.bc_sparse_conv2d_pair(ctypes.byref(ca), ctypes.byref(cb), _grid(grid), _ptr(idx),
                                     _ptr(count), cap, _stream(stream))
     _check(st, "bc_sparse_conv2d_pair")
+
+
+def bc_sparse_spp(x, layout, rows, cols, cl, w, bias, levels, out, grid, idx, count, stream=None):
+    """rows, cols: the bin grid of each level (host sequences of equal length)."""
+    cap = 0 if idx is None else int(idx.numel())
+    g = bc_spp_geom()
+    g.levels, g.cl = len(rows), int(cl)
+    for i, (r, c) in enumerate(zip(rows, cols)):
+        g.rows[i], g.cols[i] = int(r), int(c)
+    st = _lib.bc_sparse_spp(_ptr(x), desc(x, layout), ctypes.byref(g), _ptr(w), _ptr(bias), _ptr(levels),
+                            _ptr(out), desc(out, layout), _grid(grid), _ptr(idx), _ptr(count), cap,
+                            _stream(stream))
+    _check(st, "bc_sparse_spp")
 
 
 def bc_sparse_maxpool2d(geom, x, layout, out, grid, idx, count, stream=None):

@@ -486,6 +486,70 @@ bc_status bc_sparse_conv2d_pair(const bc_conv_call *a, const bc_conv_call *b, bc
     return ok();
 }
 
+bc_status bc_sparse_spp(const void *d_in, bc_tensor in, const bc_spp_geom *spp, const void *d_w,
+                        const float *d_bias, void *d_levels, void *d_out, bc_tensor out, bc_grid g,
+                        const int32_t *d_idx, const int32_t *d_count, int32_t capacity, void *stream)
+{
+    if (!d_in || !spp || !d_w || !d_levels || !d_out)
+        return fail(BC_ERR_NULL, "d_in, spp, d_w, d_levels and d_out are required");
+    bc_status st;
+    if ((st = check_tensor(in, "in"))) return st;
+    if ((st = check_tensor(out, "out"))) return st;
+    if (in.dtype != out.dtype) return fail(BC_ERR_DTYPE, "in and out dtypes differ");
+    if (in.layout != out.layout) return fail(BC_ERR_LAYOUT, "in and out layouts differ");
+    if (in.layout != BC_NHWC || in.dtype == BC_F32)
+        return fail(BC_ERR_UNSUPPORTED, "pyramid pooling takes channels-last BF16 or F16");
+    if (in.c % 8 || in.c > bc::kMaxSppChannels || 256 % (in.c / 8))
+        return fail(BC_ERR_UNSUPPORTED, "pyramid pooling needs c %% 8 == 0 with c / 8 dividing 256 "
+                                        "(c = %d)", in.c);
+    if (spp->levels < 1 || spp->levels > bc::kMaxSppLevels)
+        return fail(BC_ERR_SHAPE, "levels must be 1..%d (got %d)", bc::kMaxSppLevels, spp->levels);
+    if (spp->cl < 8 || spp->cl > 256 || spp->cl % 8)
+        return fail(BC_ERR_SHAPE, "cl must be a multiple of 8 in 8..256 (got %d)", spp->cl);
+    bc::SppGeom G;
+    G.first[0] = 0;
+    for (int l = 0; l < spp->levels; ++l) {
+        if (spp->rows[l] < 1 || spp->rows[l] > in.h || spp->cols[l] < 1 || spp->cols[l] > in.w)
+            return fail(BC_ERR_SHAPE, "level %d: %d x %d bins on a %d x %d map", l, spp->rows[l],
+                        spp->cols[l], in.h, in.w);
+        G.rows[l] = spp->rows[l];
+        G.cols[l] = spp->cols[l];
+        G.first[l + 1] = G.first[l] + spp->rows[l] * spp->cols[l];
+    }
+    if (out.n != in.n || out.h != in.h || out.w != in.w || out.c != in.c + spp->levels * spp->cl)
+        return fail(BC_ERR_SHAPE, "out must be [n][h][w][c + levels * cl] = [%d][%d][%d][%d]", in.n,
+                    in.h, in.w, in.c + spp->levels * spp->cl);
+    LayerGeom L;
+    if ((st = block_geom(out, g, L))) return st;
+    if ((st = check_index(d_idx, d_count, capacity, L.total_blocks))) return st;
+    const int es = esize_of(in.dtype);
+    const size_t wbytes = (size_t)spp->levels * spp->cl * in.c * es;
+    const size_t lbytes = (size_t)in.n * G.first[spp->levels] * spp->cl * es;
+    const size_t obytes = tensor_bytes(out), ibytes = tensor_bytes(in);
+    if (obytes >= ((size_t)1 << 31) || ibytes >= ((size_t)1 << 31) || lbytes >= ((size_t)1 << 31))
+        return fail(BC_ERR_UNSUPPORTED, "tensors of 2 GiB or more");
+    if (overlap(d_out, obytes, d_in, ibytes)) return fail(BC_ERR_ALIAS, "d_out overlaps d_in");
+    if (overlap(d_out, obytes, d_levels, lbytes) || overlap(d_levels, lbytes, d_in, ibytes) ||
+        overlap(d_levels, lbytes, d_w, wbytes) || overlap(d_levels, lbytes, d_bias, (size_t)spp->levels * spp->cl * 4))
+        return fail(BC_ERR_ALIAS, "d_levels overlaps another tensor");
+    if (overlap(d_out, obytes, d_w, wbytes) || overlap(d_out, obytes, d_bias, (size_t)spp->levels * spp->cl * 4))
+        return fail(BC_ERR_ALIAS, "d_out overlaps the weights or biases");
+    if (d_idx && (overlap(d_out, obytes, d_idx, (size_t)capacity * 4) || overlap(d_out, obytes, d_count, 4) ||
+                  overlap(d_levels, lbytes, d_idx, (size_t)capacity * 4) || overlap(d_levels, lbytes, d_count, 4)))
+        return fail(BC_ERR_ALIAS, "an output overlaps the index");
+    if ((st = check_registered(d_out, out, d_idx != nullptr))) return st;
+    G.n = in.n; G.h = in.h; G.w = in.w; G.c = in.c; G.vpp = in.c / 8;
+    G.levels = spp->levels; G.cl = spp->cl; G.cout = out.c;
+    G.gh = L.gh; G.gw = L.gw; G.bh = L.bh; G.bw = L.bw; G.total_blocks = L.total_blocks;
+    G.in_bytes = (int)ibytes; G.w_bytes = (int)wbytes; G.lv_bytes = (int)lbytes; G.out_bytes = (int)obytes;
+    hipError_t e = bc::launch_spp((const uint16_t *)d_in, (const uint16_t *)d_w, d_bias,
+                                  (uint16_t *)d_levels, (uint16_t *)d_out, G, in.dtype == BC_BF16,
+                                  d_idx, d_count, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "pyramid pooling launch");
+    if (!d_idx) mark_full(d_out);
+    return ok();
+}
+
 bc_status bc_sparse_maxpool2d(const bc_conv *geom, const void *d_in, bc_tensor in, void *d_out,
                               bc_tensor out, bc_grid g, const int32_t *d_idx,
                               const int32_t *d_count, int32_t capacity, void *stream)

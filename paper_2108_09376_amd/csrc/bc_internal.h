@@ -90,6 +90,23 @@ hipError_t launch_upsample_add(const void *coarse, const void *skip, void *out, 
                                int hc, int wc, int esize, bool nhwc, bool bf16, int gh, int gw,
                                const int32_t *idx, const int32_t *count, int relu, hipStream_t s);
 
+// Pyramid pooling (k_spp.hip): levels computed densely from the whole input map, then
+// the executed blocks of the concatenation [input, upsampled levels]. Channels last,
+// bf16/fp16; c % 8 == 0 with c / 8 dividing 256 (c <= kMaxSppChannels), cl % 8 == 0.
+constexpr int kMaxSppLevels = 8;
+constexpr int kMaxSppChannels = 2048;
+struct SppGeom {
+    int n, h, w, c, vpp;                       // input [n][h][w][c], vpp = c / 8
+    int levels, cl, cout;                      // cout = c + levels * cl
+    int rows[kMaxSppLevels], cols[kMaxSppLevels];
+    int first[kMaxSppLevels + 1];              // first bin of each level; first[levels] = bins
+    int gh, gw, bh, bw, total_blocks;          // output blocks
+    int in_bytes, w_bytes, lv_bytes, out_bytes;
+};
+hipError_t launch_spp(const uint16_t *in, const uint16_t *w, const float *bias, uint16_t *levels,
+                      uint16_t *out, const SppGeom &g, bool bf16, const int32_t *idx,
+                      const int32_t *count, hipStream_t s);
+
 // Policy network input S_t at a quarter of the frame resolution (32 channels) and the
 // block probabilities from the head's logits (channel 0 of c).
 hipError_t launch_policy_input(const void *frame, const void *state, const void *scores,

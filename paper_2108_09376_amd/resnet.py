@@ -15,12 +15,14 @@ index handed in, e.g. from bc_sample_execution_grid) and one library call per la
 nothing runs on the host in between.
 
 Segmentation network (Section 4: a SwiftNet-style single-scale model): the backbone as
-encoder, then a decoder from stride 32 up to stride 4 in which every level upsamples
-the coarser decoder feature by two (bc_sparse_upsample_add), adds a 1x1 projection of
-the encoder feature at that stride and blends with a 3x3 convolution; a 1x1 head gives
-the class scores at stride 4. The stride-32 context module is a 1x1 projection here
-(pooling over the whole image does not decompose into blocks), and the head computes
-64 channels per started 64 classes, the first `classes` being the scores.
+encoder, a spatial pyramid pooling module on its stride-32 output (a 1x1 bottleneck;
+levels with 8, 4, 2 and 1 rows of bins, each pooled densely from the whole current
+bottleneck buffer and projected by a 1x1 convolution, upsampled and concatenated at the
+executed blocks, bc_sparse_spp; a 1x1 fuse), then a decoder from stride 32 up to stride
+4 in which every level upsamples the coarser decoder feature by two
+(bc_sparse_upsample_add), adds a 1x1 projection of the encoder feature at that stride
+and blends with a 3x3 convolution; a 1x1 head gives the class scores at stride 4. The
+head computes 64 channels per started 64 classes, the first `classes` being the scores.
 """
 from __future__ import annotations
 
@@ -34,7 +36,8 @@ from . import bc
 
 @dataclass
 class Layer:
-    kind: str                  # "conv", "pool" or "up" (upsample src by 2, add res)
+    kind: str                  # "conv", "pool", "up" (upsample src by 2, add res) or
+                               # "spp" (pyramid pooling; params: grid rows, cl)
     name: str
     src: int                   # producing layer, -1 = the frame
     cin: int
@@ -82,12 +85,23 @@ def build_layers(depth: int) -> list[Layer]:
     return L
 
 
+SPP_ROWS = (8, 4, 2, 1)      # rows of the pyramid levels' bin grids
+
+
+def spp_grid(h: int, w: int, rows: int) -> tuple[int, int]:
+    """Bins of a pyramid level with `rows` rows on an h x w map: rows (at most h) by
+    rows * w / h rounded half up (1..w), about square bins on wide maps."""
+    r = min(rows, h)
+    return r, min(w, max(1, (2 * rows * w + h) // (2 * h)))
+
+
 def build_swiftnet_layers(depth: int = 18, classes: int = 19, width: int = 128) -> list[Layer]:
     """Encoder (the backbone of build_layers) followed by the decoder, in execution
-    order: dec.proj4 (1x1 on the stride-32 output), then per level s = 3, 2, 1 the
-    lateral dec.lat{s} (1x1 on the last output of encoder stage s), dec.up{s}
-    (coarser decoder feature upsampled by two plus the lateral) and dec.blend{s} (3x3);
-    then dec.logits (1x1, no ReLU)."""
+    order: dec.spp.bottleneck (1x1 on the stride-32 output), dec.spp (pyramid pooling,
+    concatenating width/4 channels per level after the bottleneck), dec.spp.fuse (1x1
+    back to `width`), then per level s = 3, 2, 1 the lateral dec.lat{s} (1x1 on the last
+    output of encoder stage s), dec.up{s} (coarser decoder feature upsampled by two plus
+    the lateral) and dec.blend{s} (3x3); then dec.logits (1x1, no ReLU)."""
     L = build_layers(depth)
     grow = 4 if depth == 50 else 1
     last = {}
@@ -99,7 +113,11 @@ def build_swiftnet_layers(depth: int = 18, classes: int = 19, width: int = 128) 
         L.append(layer)
         return len(L) - 1
 
-    x = add(Layer("conv", "dec.proj4", last[4], 512 * grow, width, 1, 1))
+    b = add(Layer("conv", "dec.spp.bottleneck", last[4], 512 * grow, width, 1, 1))
+    cl = width // 4
+    cat = width + len(SPP_ROWS) * cl
+    spp = add(Layer("spp", "dec.spp", b, width, cat, 1, 1, params=dict(rows=SPP_ROWS, cl=cl)))
+    x = add(Layer("conv", "dec.spp.fuse", spp, cat, width, 1, 1))
     for s in (3, 2, 1):
         lat = add(Layer("conv", f"dec.lat{s}", last[s], (32 << s) * grow, width, 1, 1))
         up = add(Layer("up", f"dec.up{s}", x, width, width, 1, 1, relu=False, res=lat))
@@ -110,40 +128,57 @@ def build_swiftnet_layers(depth: int = 18, classes: int = 19, width: int = 128) 
 
 def default_params(layers: list[Layer], seed0: int = 1000, bn_random: bool = False):
     """He-normal fp32 OIHW weights (seed seed0 + layer position) and batch-norm
-    statistics (identity unless bn_random), drawn by the shared input generators."""
+    statistics (identity unless bn_random), drawn by the shared input generators; a
+    pyramid pooling layer gets one set per level (1x1, cl x cin), in level order."""
     import synth
     out = []
-    for i, l in enumerate(layers):
-        if l.kind != "conv":
-            out.append(None)
-            continue
-        r = synth.rng(seed0 + i)
-        w = synth.he_normal(r, l.cout, l.cin, l.k, l.k)
-        c = l.cout
+
+    def one(r, cout, cin, k):
+        w = synth.he_normal(r, cout, cin, k, k)
         if bn_random:
-            bn = dict(gamma=r.uniform(0.5, 1.5, c), beta=r.normal(0, 0.1, c),
-                      mean=r.normal(0, 0.1, c), var=r.uniform(0.5, 1.5, c))
+            bn = dict(gamma=r.uniform(0.5, 1.5, cout), beta=r.normal(0, 0.1, cout),
+                      mean=r.normal(0, 0.1, cout), var=r.uniform(0.5, 1.5, cout))
         else:
-            bn = dict(gamma=np.ones(c), beta=np.zeros(c), mean=np.zeros(c), var=np.ones(c))
-        out.append(dict(w=w, **bn))
+            bn = dict(gamma=np.ones(cout), beta=np.zeros(cout), mean=np.zeros(cout), var=np.ones(cout))
+        return dict(w=w, **bn)
+
+    for i, l in enumerate(layers):
+        r = synth.rng(seed0 + i)
+        if l.kind == "conv":
+            out.append(one(r, l.cout, l.cin, l.k))
+        elif l.kind == "spp":
+            out.append(dict(levels=[one(r, l.params["cl"], l.cin, 1) for _ in l.params["rows"]]))
+        else:
+            out.append(None)
     return out
 
 
 def device_weights(layers: list[Layer], params, dtype, device):
     """Batch norm folded into each conv (bc_fold_bn) and the weights repacked to the
     channels-last layout in `dtype` (bc_repack_weights), on the device; None for layers
-    without weights."""
+    without weights. A pyramid pooling layer's levels are stacked: weights
+    [levels][cl][cin], biases [levels][cl]."""
     dcode = bc.BC_BF16 if dtype == torch.bfloat16 else bc.BC_F16
+
+    def fold(p):
+        wf, bf = bc.bc_fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
+        wr = bc.bc_repack_weights(wf.reshape(p["w"].shape), dcode)
+        return torch.from_numpy(wr.view(np.int16)).view(dtype), torch.from_numpy(bf)
+
     weights, biases = [], []
     for l, p in zip(layers, params):
-        if l.kind != "conv":
+        if l.kind == "conv":
+            w, b = fold(p)
+        elif l.kind == "spp":
+            parts = [fold(q) for q in p["levels"]]
+            w = torch.stack([q[0].reshape(l.params["cl"], l.cin) for q in parts])
+            b = torch.stack([q[1] for q in parts])
+        else:
             weights.append(None)
             biases.append(None)
             continue
-        wf, bf = bc.bc_fold_bn(p["w"], None, p["gamma"], p["beta"], p["mean"], p["var"], 1e-5)
-        wr = bc.bc_repack_weights(wf.reshape(p["w"].shape), dcode)
-        weights.append(torch.from_numpy(wr.view(np.int16)).view(dtype).to(device).contiguous())
-        biases.append(torch.from_numpy(bf).to(device))
+        weights.append(w.to(device).contiguous())
+        biases.append(b.to(device).contiguous())
     return weights, biases
 
 
@@ -328,6 +363,16 @@ class SparseResNet:
         self.buffers = [torch.empty((1, oh, ow, c), dtype=dtype, device=self.device)
                         for (oh, ow, c) in self.shapes]
         self.handles = [bc.Buffer(t, bc.BC_NHWC) for t in self.buffers]
+        # pyramid pooling: each level's bin grid on its map, and the level buffer the
+        # library rewrites every frame
+        self.spp = {}
+        for i, l in enumerate(self.layers):
+            if l.kind == "spp":
+                ih, iw, _ = self.shapes[l.src]
+                bins = [spp_grid(ih, iw, r) for r in l.params["rows"]]
+                lv = torch.empty((1, sum(a * b for a, b in bins), l.params["cl"]), dtype=dtype,
+                                 device=self.device)
+                self.spp[i] = (bins, lv)
         nblk = self.grid[0] * self.grid[1]
         self.idx = torch.zeros(nblk, dtype=torch.int32, device=self.device)
         self.count = torch.zeros(1, dtype=torch.int32, device=self.device)
@@ -422,6 +467,11 @@ class SparseResNet:
         elif l.kind == "up":
             bc.bc_sparse_upsample_add(src, bc.BC_NHWC, self.buffers[l.res], out, self.grid,
                                       int(l.relu), idx, cnt, stream)
+        elif l.kind == "spp":
+            bins, lv = self.spp[i]
+            bc.bc_sparse_spp(src, bc.BC_NHWC, [a for a, _ in bins], [b for _, b in bins],
+                             l.params["cl"], self.weights[i], self.biases[i], lv, out, self.grid,
+                             idx, cnt, stream)
         else:
             res = None if l.res is None else self.buffers[l.res]
             bc.bc_sparse_conv2d((l.k, l.k, l.stride, l.pad, int(l.relu)), src, bc.BC_NHWC,

@@ -490,3 +490,40 @@ def test_noalloc_scratch_holds_every_network_layer(B, net):
             continue                       # the stem's input is the frame (3 channels)
         st, msg = _fits_scratch(B, l, shapes[l.src], (8, 16))
         assert st != B.BC_ERR_CAPACITY, (net, l.name, msg)
+
+
+def spp_call(B, inp=(1, 128, 32, 64, 1, 1), out=(1, 256, 32, 64, 1, 1), levels=4, cl=32,
+             rows=(8, 4, 2, 1), cols=(16, 8, 4, 2), grid=(8, 16), d_in=FAKE_IN, d_w=FAKE_W,
+             d_lv=FAKE_RES, d_out=FAKE_OUT, d_idx=FAKE_IDX, d_cnt=FAKE_CNT, cap=128):
+    lib = B.raw()
+    g = B.bc_spp_geom()
+    g.levels, g.cl = levels, cl
+    for i, (r, c) in enumerate(zip(rows, cols)):
+        g.rows[i], g.cols[i] = r, c
+    st = lib.bc_sparse_spp(d_in, B.bc_tensor(*inp), ctypes.byref(g), d_w, None, d_lv, d_out,
+                           B.bc_tensor(*out), B.bc_grid(*grid), d_idx, d_cnt, cap, None)
+    return st, B.bc_last_error()
+
+
+@no_gpu
+def test_spp_validation_codes(B):
+    E = B
+    assert spp_call(B, d_lv=None)[0] == E.BC_ERR_NULL
+    assert spp_call(B, d_w=None)[0] == E.BC_ERR_NULL
+    assert spp_call(B, out=(1, 255, 32, 64, 1, 1))[0] == E.BC_ERR_SHAPE          # c + levels * cl
+    assert spp_call(B, out=(1, 256, 16, 64, 1, 1))[0] == E.BC_ERR_SHAPE
+    assert spp_call(B, levels=0)[0] == E.BC_ERR_SHAPE
+    assert spp_call(B, levels=9)[0] == E.BC_ERR_SHAPE
+    assert spp_call(B, cl=12, out=(1, 176, 32, 64, 1, 1))[0] == E.BC_ERR_SHAPE
+    assert spp_call(B, rows=(33, 4, 2, 1))[0] == E.BC_ERR_SHAPE                    # more rows than h
+    assert spp_call(B, cols=(16, 8, 4, 0))[0] == E.BC_ERR_SHAPE
+    assert spp_call(B, inp=(1, 128, 32, 64, 2, 1))[0] == E.BC_ERR_DTYPE
+    assert spp_call(B, inp=(1, 128, 32, 64, 1, 0), out=(1, 256, 32, 64, 1, 0))[0] == E.BC_ERR_UNSUPPORTED
+    assert spp_call(B, inp=(1, 96, 32, 64, 1, 1), out=(1, 224, 32, 64, 1, 1))[0] == E.BC_ERR_UNSUPPORTED
+    assert spp_call(B, grid=(7, 16))[0] == E.BC_ERR_NOT_DIVISIBLE
+    assert spp_call(B, cap=100)[0] == E.BC_ERR_CAPACITY
+    assert spp_call(B, d_out=FAKE_IN + 64)[0] == E.BC_ERR_ALIAS
+    assert spp_call(B, d_lv=FAKE_IN)[0] == E.BC_ERR_ALIAS
+    assert spp_call(B, d_lv=FAKE_OUT + 2)[0] == E.BC_ERR_ALIAS
+    # a well-formed call passes every check and fails only at the launch (no GPU here)
+    assert spp_call(B)[0] == E.BC_ERR_HIP

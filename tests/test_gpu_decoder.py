@@ -201,3 +201,78 @@ def test_information_gain_copied_blocks_are_zero(B):
     want = P.seg_information_gain(synth.storage_to_f64(lt[:, :classes], dtype),
                                   synth.storage_to_f64(lp[:, :classes], dtype), *grid)
     assert max_abs_rel(got, want) <= 1e-4
+
+
+# ------------------------------------------------------------------ pyramid pooling
+
+@pytest.mark.parametrize("dtype,n,c,h,w,grid,rows,cl,p", [
+    ("bf16", 1, 128, 32, 64, (8, 16), (8, 4, 2, 1), 32, 0.3),   # the 2048x1024 workload
+    ("bf16", 2, 16, 12, 20, (3, 5), (5, 3, 1), 8, 0.5),         # bins of unequal size
+    ("f16", 1, 8, 8, 16, (2, 4), (8, 4, 2, 1), 16, 0.6),        # one vector per pixel
+    ("bf16", 1, 512, 8, 16, (2, 4), (3, 2), 64, 0.5),           # 64 vectors per pixel
+    ("bf16", 1, 2048, 4, 8, (2, 2), (1,), 8, 1.0),              # the widest input
+])
+def test_spp_parity(B, dtype, n, c, h, w, grid, rows, cl, p):
+    r = synth.rng(350 + c + h)
+    gh, gw = grid
+    bins = [oracle.spp_bins(h, w, g) for g in rows]
+    x = synth.to_storage_bits(synth.normal(r, (n, c, h, w)), dtype)
+    wts = [synth.to_storage_bits(synth.he_normal(r, cl, c, 1, 1), dtype) for _ in rows]
+    bias = [synth.normal(r, cl, 0.1).astype(np.float32) for _ in rows]
+    cout = c + len(rows) * cl
+    prev = synth.nan_canaries(r, (n, cout, h, w), dtype)
+    mask = synth.bernoulli_mask(r, n, gh, gw, p)
+    want_lv = oracle.spp_levels(x, rows, wts, bias, dtype)
+    want = oracle.sparse_spp(x, want_lv, mask, prev, dtype)
+    idx, cnt = _index(B, mask)
+    wd = torch.from_numpy(np.stack([wl.reshape(cl, c) for wl in wts]).view(np.int16)).cuda()
+    wd = wd.view(torch.bfloat16 if dtype == "bf16" else torch.float16)
+    bd = torch.from_numpy(np.stack(bias)).cuda()
+    tb = sum(a * b for a, b in bins)
+    lv = torch.full((n, tb, cl), float("nan"), device="cuda").to(wd.dtype)
+    out = to_dev(prev, dtype)
+    B.bc_sparse_spp(to_dev(x, dtype), B.BC_NHWC, [a for a, _ in bins], [b for _, b in bins], cl, wd, bd,
+                    lv, out, grid, idx, cnt)
+    torch.cuda.synchronize()
+    # levels: every bin of every image, [n][bins][cl]
+    got_lv = lv.view(torch.int16).cpu().numpy().view(np.uint16)
+    o = 0
+    for (a, b), wl in zip(bins, want_lv):
+        g = got_lv[:, o:o + a * b].reshape(n, a, b, cl).transpose(0, 3, 1, 2)
+        assert max_abs_rel(oracle.value(g, dtype), oracle.value(wl, dtype)) <= TOL[dtype]
+        o += a * b
+    got = from_dev(out)
+    sel = block_select(mask, got.shape)
+    assert np.array_equal(got[~sel], prev[~sel]), "copied blocks changed"
+    assert np.array_equal(got[:, :c][sel[:, :c]], x[sel[:, :c]])      # the input's own bits
+    # the context channels against the oracle's resampling of the GPU's own levels (the
+    # resampling alone) and of the oracle's levels (the whole layer)
+    own = oracle.sparse_spp(x, [got_lv[:, sum(a * b for a, b in bins[:k]):sum(a * b for a, b in bins[:k + 1])]
+                                .reshape(n, bins[k][0], bins[k][1], cl).transpose(0, 3, 1, 2).copy()
+                                for k in range(len(bins))], mask, prev, dtype)
+    # fp32 weights of non-dyadic resampling ratios may put a value on the other side of
+    # one rounding boundary: at most one unit in the last place of the storage format
+    ulp = {"bf16": 2.0 ** -7, "f16": 2.0 ** -10}[dtype]
+    assert max_abs_rel(oracle.value(got[sel], dtype), oracle.value(own[sel], dtype)) <= ulp
+    assert max_abs_rel(oracle.value(got[sel], dtype), oracle.value(want[sel], dtype)) <= TOL[dtype]
+
+
+def test_spp_no_block_and_every_block(B):
+    """An empty grid writes no output element (the levels are still recomputed); the
+    full call (no index) writes every block."""
+    r = synth.rng(360)
+    c, h, w, cl = 64, 16, 32, 16
+    x = synth.to_storage_bits(synth.normal(r, (1, c, h, w)), "bf16")
+    wb = synth.to_storage_bits(synth.he_normal(r, 2 * cl, c, 1, 1), "bf16").reshape(2, cl, c)
+    wd = torch.from_numpy(wb.view(np.int16)).view(torch.bfloat16).cuda()
+    prev = synth.nan_canaries(r, (1, c + 2 * cl, h, w), "bf16")
+    out = to_dev(prev, "bf16")
+    lv = torch.empty((1, 4 * 8 + 1 * 2, cl), dtype=torch.bfloat16, device="cuda")
+    idx, cnt = _index(B, np.zeros((1, 4, 8), np.uint8))
+    B.bc_sparse_spp(to_dev(x, "bf16"), B.BC_NHWC, [4, 1], [8, 2], cl, wd, None, lv, out, (4, 8), idx, cnt)
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(out), prev)
+    B.bc_sparse_spp(to_dev(x, "bf16"), B.BC_NHWC, [4, 1], [8, 2], cl, wd, None, lv, out, (4, 8), None, None)
+    torch.cuda.synchronize()
+    got = from_dev(out)
+    assert np.array_equal(got[:, :c], x) and not np.isnan(oracle.value(got, "bf16")).any()

@@ -2,7 +2,7 @@
 at a time, with all of the layer's inputs drawn on the host (no GPU value enters the
 oracle).
 
-For ResNet-50 and SwiftNet-18 at 2048x1024 (128-pixel blocks, 38 of the 128 blocks
+For ResNet-50, SwiftNet-18 and SwiftNet-50 at 2048x1024 (128-pixel blocks, 38 of the 128 blocks
 active, clustered): the layer's input, residual and previous output are drawn seeded on
 the host and uploaded into the runner's own persistent buffers, the oracle's folded
 weights into the runner's weight tensors; the layer then runs alone through the runner
@@ -12,7 +12,7 @@ index, in the launch configuration of the benchmark's frame. Checked (Section 3.
 * active outputs of convolutions match the oracle's dense definition within 2e-2 max
   abs-rel on sampled points (computed one by one at full size); max pooling on every
   active output bit for bit (a maximum of stored values is exact); the decoder's
-  upsample-add on every active output within 2e-2.
+  upsample-add and pyramid pooling on every active output within 2e-2.
 Also: the frame with and without paired launches gives the same bits in every buffer,
 and every layer of the policy network (Section 3.3) is held element-wise at the
 workload's size.
@@ -29,7 +29,8 @@ from tests._util import block_select, from_dev, max_abs_rel, to_dev, weights_dev
 pytestmark = pytest.mark.gpu
 
 H, W, GH, GW = 1024, 2048, 8, 16
-TABLES = {"resnet50": onet.resnet_table(50), "swiftnet18": onet.swiftnet_table(18)}
+TABLES = {"resnet50": onet.resnet_table(50), "swiftnet18": onet.swiftnet_table(18),
+          "swiftnet50": onet.swiftnet_table(50)}
 SAMPLES = 2000
 
 
@@ -56,9 +57,15 @@ def _net(R, kind):
     if kind == "resnet50":
         net = resnet.SparseResNet(50, H, W, 128, params=params)
     else:
-        net = resnet.SparseSwiftNet(18, H, W, 128, params=params)
+        net = resnet.SparseSwiftNet(int(kind[-2:]), H, W, 128, params=params)
     for i, f in enumerate(folded):
-        if f is not None:                            # the oracle's own weight bits
+        if f is None:
+            continue
+        if "levels" in f:                            # pyramid pooling: [levels][cl][c]
+            wl = np.stack([q["w_bits"].reshape(q["w_bits"].shape[:2]) for q in f["levels"]])
+            net.weights[i].copy_(torch.from_numpy(wl.view(np.int16)).view(torch.bfloat16).cuda())
+            net.biases[i].copy_(torch.from_numpy(np.stack([q["bias"] for q in f["levels"]])).cuda())
+        else:                                        # the oracle's own weight bits
             net.weights[i].copy_(weights_dev(f["w_bits"], "bf16"))
             net.biases[i].copy_(torch.from_numpy(f["bias"]).cuda())
     x = to_dev(synth.to_storage_bits(synth.normal(synth.rng(1), (1, 3, H, W)), "bf16"), "bf16")
@@ -98,6 +105,13 @@ def _check_layer(net, table, folded, mask, li, src_bits, res_bits, prev_bits, go
         err = max_abs_rel(oracle.value(got[sel], "bf16"), oracle.value(want[sel], "bf16"))
         assert err <= 2e-2, err
         return err
+    if l["kind"] == "spp":
+        lv = folded[li]["levels"]
+        levels = oracle.spp_levels(src_bits, l["grid"], [q["w_bits"] for q in lv], [q["bias"] for q in lv], "bf16")
+        want = oracle.sparse_spp(src_bits, levels, mask, prev_bits, "bf16")
+        err = max_abs_rel(oracle.value(got[sel], "bf16"), oracle.value(want[sel], "bf16"))
+        assert err <= 2e-2, err
+        return err
     act = np.argwhere(sel)
     pick = act[synth.rng(7000 + li).choice(len(act), size=min(SAMPLES, len(act)), replace=False)]
     z = oracle.conv2d_points(oracle.value(src_bits, "bf16"), oracle.value(folded[li]["w_bits"], "bf16"),
@@ -122,14 +136,15 @@ def test_layer_teacher_forced_full_size(R, kind, li):
     partner = net.pairs.get(li)
     first = next((i for i, j in net.pairs.items() if j == li), None)
     group = [li] if partner is None and first is None else sorted([li, partner if partner is not None else first])
-    l0 = table[group[0]]
-    src_shape = (1, 3, H, W) if l0["src"] < 0 else (1,) + sh[l0["src"]]
-    src_bits = _draw_map(5000 + group[0], src_shape)
-    if l0["src"] < 0:
-        x.copy_(to_dev(src_bits, "bf16"))
-    else:
-        net.buffers[l0["src"]].copy_(to_dev(src_bits, "bf16"))
-    res, prev = {}, {}
+    # every input of the launch: the layers' sources (paired layers may read different
+    # buffers, e.g. a decoder lateral beside the pyramid's bottleneck), residuals and
+    # previous outputs, drawn on the host and uploaded
+    srcs, res, prev = {}, {}, {}
+    for i in group:
+        si = table[i]["src"]
+        if si not in srcs:
+            srcs[si] = _draw_map(5000 + (si if si >= 0 else 999), (1, 3, H, W) if si < 0 else (1,) + sh[si])
+            (x if si < 0 else net.buffers[si]).copy_(to_dev(srcs[si], "bf16"))
     for i in group:
         l = table[i]
         if l["res"] is not None:
@@ -137,6 +152,8 @@ def test_layer_teacher_forced_full_size(R, kind, li):
             net.buffers[l["res"]].copy_(to_dev(res[i], "bf16"))
         prev[i] = synth.nan_canaries(synth.rng(5600 + i), (1,) + sh[i], "bf16")
         net.buffers[i].copy_(to_dev(prev[i], "bf16"))
+    src_bits = srcs[table[li]["src"]]
+    src_shape = src_bits.shape
     print(kind, li, [table[i]["name"] for i in group], src_shape, flush=True)
     if len(group) == 2:
         net.run_pair(group[0], group[1], x, net.idx, net.count)
