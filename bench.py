@@ -63,6 +63,8 @@ def parse():
                     help="run only the standalone gather/scatter cases for a rocprofv3 --pmc run")
     ap.add_argument("--gs-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the gather/scatter traffic table of two rocprofv3 --pmc runs")
+    ap.add_argument("--cpu-configs", action="store_true",
+                    help="time the CPU oracle on configurations 1, 2, 4 and 5 (both modes) and exit")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the HBM-traffic summary of two counter_collection.csv files and exit")
     ap.add_argument("--rocprof-summary", nargs="+", metavar="CSV",
@@ -71,12 +73,32 @@ def parse():
     return ap.parse_args()
 
 
+def cpu_model():
+    """The host CPU's model name and thread count as the kernel reports them."""
+    name, fam, mod = "unknown", "?", "?"
+    try:
+        for line in open("/proc/cpuinfo"):
+            k, _, v = line.partition(":")
+            k, v = k.strip(), v.strip()
+            if k == "model name" and name == "unknown":
+                name = v
+            elif k == "cpu family" and fam == "?":
+                fam = v
+            elif k == "model" and mod == "?":
+                mod = v
+    except OSError:
+        pass
+    return f"{name} (family {fam}, model {mod}), {os.cpu_count()} logical CPUs"
+
+
 def cpu_baseline(mask):
     """The CPU oracle (dense convolution then masked select, fp64, OpenMP) on a bounded
     sample of the workload: every convolution of ResNet-50's first two stages (layer1
     and layer2: 23 convs, stride 4 and 8) at their real sizes for a 2048x1024 frame, with
     the frame's mask; each layer gets seeded bf16 inputs of its shape. Rate = the
-    sample's active-block FLOPs / oracle time."""
+    sample's active-block FLOPs / oracle time. Beside it, the oracle's only-active mode
+    on the same sample (same arithmetic, inactive blocks skipped: the fair sparse CPU
+    comparison) and the configuration-1 layer (fp32, two frames) in both modes."""
     import numpy as np
 
     import oracle
@@ -89,7 +111,7 @@ def cpu_baseline(mask):
     act = int((mask != 0).sum()) / (gh * gw)
     flops = 0.0
     n = 0
-    dt = 0.0
+    dt = dt_act = 0.0
     for i, l in enumerate(layers):
         if l.kind != "conv" or not l.name.startswith(("layer1", "layer2")):
             continue
@@ -99,17 +121,164 @@ def cpu_baseline(mask):
         wt = synth.to_storage_bits(synth.he_normal(r, l.cout, l.cin, l.k, l.k), "bf16")
         prev = np.zeros((1, l.cout, oh, ow), np.uint16)
         rb = synth.to_storage_bits(synth.normal(r, (1, l.cout, oh, ow)), "bf16") if l.res is not None else None
+        args = (x, wt, mask, prev, "bf16", l.stride, l.pad, np.zeros(l.cout, np.float32), rb, l.relu)
         t0 = time.perf_counter()           # the oracle only, not the input generation
-        oracle.sparse_conv2d(x, wt, mask, prev, "bf16", l.stride, l.pad, np.zeros(l.cout, np.float32), rb,
-                             l.relu)
-        dt += time.perf_counter() - t0
+        oracle.sparse_conv2d(*args)
+        t1 = time.perf_counter()
+        oracle.sparse_conv2d_active(*args)
+        dt_act += time.perf_counter() - t1
+        dt += t1 - t0
         flops += 2.0 * l.cin * l.cout * l.k * l.k * oh * ow * act
         n += 1
+    c1 = config1_cpu()
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"ResNet-50 layer1 + layer2 ({n} convs) at their 2048x1024-frame sizes, bf16 "
                       f"values, dense-then-select in fp64, {int((mask != 0).sum())}/{gh * gw} blocks "
-                      f"active; {dt:.1f} s"}
+                      f"active; {dt:.1f} s",
+            "cpu_model": cpu_model(),
+            "only_active": {"value": round(flops / dt_act / 1e12, 6), "unit": "TFLOP/s",
+                            "seconds": round(dt_act, 2)},
+            "config1_us_per_frame": c1,
+            "configs_recorded": recorded_cpu_configs()}
+
+
+def config1_inputs():
+    """Configuration 1: NCHW fp32 [1, 16, 64, 128], 3x3 16 -> 16, 8x16 grid of 8x8
+    blocks, He-normal weights, N(0, 1) inputs and previous output, two frames with
+    independent Bernoulli(0.25) grids."""
+    import synth
+    r = synth.rng(synth.SEED_INPUT)
+    xs = [synth.to_storage_bits(synth.normal(r, (1, 16, 64, 128)), "f32") for _ in range(2)]
+    wt = synth.to_storage_bits(synth.he_normal(synth.rng(synth.SEED_WEIGHT0), 16, 16, 3, 3), "f32")
+    prev = synth.to_storage_bits(synth.normal(synth.rng(synth.SEED_PREV), (1, 16, 64, 128)), "f32")
+    masks = [synth.bernoulli_mask(synth.rng(synth.SEED_MASK0 + t), 1, 8, 16, 0.25) for t in range(2)]
+    return xs, wt, prev, masks
+
+
+def config1_cpu():
+    """The oracle on configuration 1's two frames (frame 1 on frame 0's output), both
+    modes: microseconds per frame."""
+    import oracle
+    xs, wt, prev, masks = config1_inputs()
+    out = {}
+    for mode, fn in (("dense_then_select", oracle.sparse_conv2d), ("only_active", oracle.sparse_conv2d_active)):
+        y = prev
+        t0 = time.perf_counter()
+        for x, m in zip(xs, masks):
+            y = fn(x, wt, m, y, "f32", 1, 1, None, None, True)
+        out[mode] = round((time.perf_counter() - t0) / 2 * 1e6, 1)
+    return out
+
+
+def config1_gpu(torch, bc, dev):
+    """Configuration 1 on the GPU (fp32 NCHW path): one frame = index build + the layer,
+    captured as a graph of 10 frames; microseconds per frame."""
+    import numpy as np
+    xs, wt, prev, masks = config1_inputs()
+    x = torch.from_numpy(xs[0].view(np.float32)).to(dev)
+    w = torch.from_numpy(wt.view(np.float32)).to(dev)
+    y = torch.from_numpy(prev.view(np.float32)).to(dev)
+    m = torch.from_numpy(masks[0]).to(dev)
+    idx = torch.empty(128, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int32, device=dev)
+
+    def frame():
+        bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
+        bc.bc_sparse_conv2d((3, 3, 1, 1, 1), x, bc.BC_NCHW, w, None, None, y, (8, 16), idx, cnt)
+
+    frame()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(10):
+            frame()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return round(e0.elapsed_time(e1) * 1e3 / 100, 2)
+
+
+CPU_CONFIGS_PROFILE = os.path.join(ROOT, "profiles", "cpu_oracle_configs.txt")
+
+
+def cpu_configs():
+    """The oracle on configurations 1, 2 and 4 (one frame each; configuration 4 every
+    one of its 18 layers) and 5 (ResNet-18 on frames 0-3 of the synthetic clip), in
+    both modes, on this host's cores. Prints a progress line per item and a summary."""
+    import numpy as np
+
+    import oracle
+    import synth
+    from oracle import network as onet
+    lines = [f"host: {cpu_model()}; oracle threads: {oracle.num_threads()}"]
+
+    def emit(s):
+        print(s, flush=True)
+        lines.append(s)
+
+    def layer(tag, cin, cout, h, w, k, mask, seed):
+        r = synth.rng(seed)
+        x = synth.to_storage_bits(synth.normal(r, (1, cin, h, w)), "bf16")
+        wt = synth.to_storage_bits(synth.he_normal(r, cout, cin, k, k), "bf16")
+        prev = synth.to_storage_bits(synth.normal(r, (1, cout, h, w)), "bf16")
+        args = (x, wt, mask, prev, "bf16", 1, k // 2, np.zeros(cout, np.float32), None, True)
+        act = int((mask != 0).sum()) / mask.size
+        res = {}
+        for mode, fn in (("dense_then_select", oracle.sparse_conv2d), ("only_active", oracle.sparse_conv2d_active)):
+            t0 = time.perf_counter()
+            fn(*args)
+            res[mode] = time.perf_counter() - t0
+        fl = 2.0 * cin * cout * k * k * h * w * act
+        emit(f"{tag:28s} dense {res['dense_then_select']:8.2f} s  only-active {res['only_active']:8.2f} s  "
+             f"active GFLOP {fl / 1e9:8.2f}")
+        return res, fl
+
+    c1 = config1_cpu()
+    emit(f"config 1 (fp32 3x3 16->16 @64x128, 2 frames): dense {c1['dense_then_select']:.1f} us/frame, "
+         f"only-active {c1['only_active']:.1f} us/frame")
+    m30 = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
+    layer("config 2 3x3 64->64 @256x512", 64, 64, 256, 512, 3, m30, 2)
+    tot = {"dense_then_select": 0.0, "only_active": 0.0}
+    tf = 0.0
+    for k in (1, 3):
+        for cin in (256, 512, 1024):
+            for cout in (256, 512, 1024):
+                res, fl = layer(f"config 4 {k}x{k} {cin}->{cout} @64x128", cin, cout, 64, 128, k, m30, 4000 + cin + cout + k)
+                for m in tot:
+                    tot[m] += res[m]
+                tf += fl
+    emit(f"config 4 all 18 layers: dense {tot['dense_then_select']:.1f} s, only-active {tot['only_active']:.1f} s "
+         f"({tf / 1e9:.1f} active GFLOP: {tf / tot['dense_then_select'] / 1e12:.5f} / "
+         f"{tf / tot['only_active'] / 1e12:.5f} TFLOP/s)")
+    table = onet.resnet_table(18)
+    folded = onet.fold_params(table, onet.make_params(table, seed0=1000), "bf16")
+    clip = synth.SyntheticClip(synth.SEED_INPUT + 4)
+    sh = onet.shapes(table, 1024, 2048)
+    for mode in ("dense_then_select", "only_active"):
+        prev = [np.zeros((1,) + s_, np.uint16) for s_ in sh]
+        ts = []
+        for t in range(4):
+            x = synth.to_storage_bits(clip.frame(t).transpose(0, 3, 1, 2).copy(), "bf16")
+            t0 = time.perf_counter()
+            prev = onet.frame(table, folded, x, clip.mask(t), prev, "bf16", only_active=(mode == "only_active"))
+            ts.append(time.perf_counter() - t0)
+            emit(f"config 5 ResNet-18 frame {t} ({mode}, {clip.mask(t).mean():.3f} active): {ts[-1]:.1f} s")
+        emit(f"config 5 {mode}: frames 0-3 {', '.join(f'{v:.1f}' for v in ts)} s, mean {sum(ts) / 4:.1f} s")
+    return "\n".join(lines)
+
+
+def recorded_cpu_configs():
+    """The per-configuration oracle timings committed under profiles/ (text lines), or None."""
+    try:
+        return [l for l in open(CPU_CONFIGS_PROFILE).read().splitlines() if l.startswith(("host", "config"))]
+    except OSError:
+        return None
 
 
 def layer_sweep(torch, bc, dev):
@@ -915,6 +1084,9 @@ def main():
     if args.gs_summary:
         print(gs_summary(*args.gs_summary))
         return
+    if args.cpu_configs:
+        print(cpu_configs())
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
@@ -1106,6 +1278,7 @@ def main():
                      "trace_conv_dispatch_window": conv_window,
                      "slowest_layers_us": {net.layers[i].name: round(u, 2) for i, u in slowest}},
     }
+    out["config1_gpu_us_per_frame"] = config1_gpu(torch, bc, dev)
     out["measured_ceilings"] = measured_ceilings(torch, dev)
     if not args.no_vendor_dense:
         vms = vendor_dense_frame(torch, dev, net.layers)

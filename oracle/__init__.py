@@ -69,6 +69,9 @@ def _lib():
         lib.oracle_conv2d_points.argtypes = [dp, i, i, i, i, dp, i, i, i, i, i, dp, dp, i, i, i,
                                              ip, ctypes.c_int64, dp]
         lib.oracle_conv2d_points.restype = None
+        lib.oracle_conv2d_blocks.argtypes = [dp, i, i, i, i, dp, i, i, i, i, i, dp, dp, i, dp, i, i,
+                                             ip, i, i, i]
+        lib.oracle_conv2d_blocks.restype = None
         lib.oracle_maxpool2d_dense.argtypes = [dp, i, i, i, i, i, i, i, dp, i, i]
         lib.oracle_maxpool2d_dense.restype = None
         lib.oracle_num_threads.argtypes = []
@@ -226,6 +229,30 @@ def sparse_conv2d(x_bits, w_bits, mask, prev_bits, dtype, stride=1, pad=0, bias=
     fresh = store(z, dtype)
     gh, gw = np.asarray(mask).shape[1:]
     return select(mask, fresh, prev_bits, z.shape[2] // gh, z.shape[3] // gw)
+
+
+def sparse_conv2d_active(x_bits, w_bits, mask, prev_bits, dtype, stride=1, pad=0, bias=None,
+                         residual_bits=None, relu=False):
+    """sparse_conv2d evaluated only where it is kept: the same per-point definition (C,
+    fp64, order ci -> i -> j) at the output points of the executed blocks, nothing
+    elsewhere, then the same rounding and select. Bit-identical to sparse_conv2d; the
+    fair CPU comparison for a block-sparse execution (it skips what the select would
+    discard)."""
+    x = np.ascontiguousarray(value(x_bits, dtype), np.float64)
+    w = np.ascontiguousarray(value(w_bits, dtype), np.float64)
+    n, cin, h, wd = x.shape
+    cout, _, kh, kw = w.shape
+    ho, wo = out_size(h, kh, stride, pad), out_size(wd, kw, stride, pad)
+    res = None if residual_bits is None else np.ascontiguousarray(value(residual_bits, dtype))
+    b = None if bias is None else np.ascontiguousarray(np.asarray(bias, np.float32).astype(np.float64))
+    gh, gw = np.asarray(mask).shape[1:]
+    blocks, nb = block_index(mask)
+    z = np.zeros((n, cout, ho, wo), np.float64)
+    if nb:
+        _lib().oracle_conv2d_blocks(_dp(x), n, cin, h, wd, _dp(w), cout, kh, kw, stride, pad, _dp(b),
+                                    _dp(res), int(bool(relu)), _dp(z), ho, wo,
+                                    blocks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), nb, gh, gw)
+    return select(mask, store(z, dtype), prev_bits, ho // gh, wo // gw)
 
 
 def sparse_maxpool2d(x_bits, mask, prev_bits, dtype, k=3, stride=2, pad=1):

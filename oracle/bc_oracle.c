@@ -86,6 +86,33 @@ void oracle_conv2d_points(const double *x, int n, int cin, int h, int w,
     }
 }
 
+/* The same definition at every output point of the listed output blocks only (the
+ * oracle's "only active" mode: identical arithmetic per point, inactive blocks
+ * skipped). Block id b = (img * gh + gy) * gw + gx covers output rows gy*bh ..
+ * gy*bh + bh - 1 and columns gx*bw .. gx*bw + bw - 1 of image img; out is the full
+ * [n][cout][ho][wo] array, written at those points only. */
+void oracle_conv2d_blocks(const double *x, int n, int cin, int h, int w,
+                          const double *wt, int cout, int kh, int kw,
+                          int stride, int pad, const double *bias,
+                          const double *residual, int relu, double *out, int ho, int wo,
+                          const int32_t *blocks, int nblocks, int gh, int gw)
+{
+    (void)n;
+    const int bh = ho / gh, bw = wo / gw;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int k = 0; k < nblocks; ++k)
+        for (int co = 0; co < cout; ++co) {
+            const int b = blocks[k];
+            const int nn = b / (gh * gw), gy = (b % (gh * gw)) / gw, gx = b % gw;
+            for (int y = gy * bh; y < (gy + 1) * bh; ++y)
+                for (int xo = gx * bw; xo < (gx + 1) * bw; ++xo) {
+                    size_t o = (((size_t)nn * cout + co) * ho + y) * (size_t)wo + xo;
+                    double acc = conv_point(x, cin, h, w, wt, kh, kw, stride, pad, nn, co, y, xo);
+                    out[o] = finish(acc, bias, residual, o, co, relu);
+                }
+        }
+}
+
 /* Dense max pooling with -inf padding (the padded positions never win). */
 void oracle_maxpool2d_dense(const double *x, int n, int c, int h, int w,
                             int k, int stride, int pad, double *out, int ho, int wo)

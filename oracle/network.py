@@ -19,8 +19,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (fold_bn, sparse_conv2d, sparse_maxpool2d, sparse_spp, sparse_upsample_add, spp_levels,
-               store)
+from . import (fold_bn, sparse_conv2d, sparse_conv2d_active, sparse_maxpool2d, sparse_spp,
+               sparse_upsample_add, spp_levels, store)
 
 
 def resnet_table(depth: int):
@@ -215,12 +215,15 @@ def shapes(table, h, w):
     return out
 
 
-def frame(table, folded, x_bits, mask, prev, dtype):
+def frame(table, folded, x_bits, mask, prev, dtype, only_active=False):
     """One frame through the block-sparse network.
 
     x_bits: the frame, NCHW bit patterns. mask: uint8 [N, Gh, Gw] execution grid.
     prev: list of previous per-layer buffers (NCHW bit patterns). Returns the new list.
+    only_active: convolutions through sparse_conv2d_active (the same bits, inactive
+    blocks not computed), for timing the fair sparse CPU comparison.
     """
+    conv = sparse_conv2d_active if only_active else sparse_conv2d
     bufs = []
     for li, l in enumerate(table):
         src = x_bits if l["src"] < 0 else bufs[l["src"]]
@@ -234,7 +237,7 @@ def frame(table, folded, x_bits, mask, prev, dtype):
             y = sparse_spp(src, levels, mask, prev[li], dtype)
         else:
             res = None if l["res"] is None else bufs[l["res"]]
-            y = sparse_conv2d(src, folded[li]["w_bits"], mask, prev[li], dtype,
+            y = conv(src, folded[li]["w_bits"], mask, prev[li], dtype,
                               stride=l["stride"], pad=l["pad"], bias=folded[li]["bias"],
                               residual_bits=res, relu=l["relu"])
         bufs.append(y)

@@ -404,3 +404,28 @@ def test_network_static_frame_bit_identical():
     for (c, hh, ww), a, b in zip(sh, f0, f2):
         sel = np.broadcast_to(oracle.expand_mask(m, hh // 2, ww // 4), a.shape)
         assert np.array_equal(a[~sel], b[~sel])
+
+
+@pytest.mark.parametrize("seed,shape,k,s,res,relu,p", [
+    (700, (1, 5, 12, 16, 7), 3, 1, True, True, 0.4),
+    (701, (2, 3, 16, 24, 4), 3, 2, False, True, 0.5),
+    (702, (1, 8, 8, 8, 8), 1, 1, True, False, 0.0),      # no block
+    (703, (1, 4, 14, 14, 6), 7, 2, False, True, 1.0),    # every block, stem-like
+])
+def test_only_active_mode_equals_dense_then_select(seed, shape, k, s, res, relu, p):
+    """The only-active mode computes the same points with the same arithmetic and skips
+    the rest: bit for bit the dense-then-select result, whatever the mask."""
+    n, cin, h, w, cout = shape
+    r = synth.rng(seed)
+    pad = k // 2
+    ho, wo = oracle.out_size(h, k, s, pad), oracle.out_size(w, k, s, pad)
+    gh, gw = (2, 2) if ho % 2 == 0 and wo % 2 == 0 else (1, 1)
+    x = synth.to_storage_bits(synth.normal(r, (n, cin, h, w)), "bf16")
+    wt = synth.to_storage_bits(synth.he_normal(r, cout, cin, k, k), "bf16")
+    bias = synth.normal(r, cout, 0.1).astype(np.float32)
+    rb = synth.to_storage_bits(synth.normal(r, (n, cout, ho, wo)), "bf16") if res else None
+    prev = synth.nan_canaries(r, (n, cout, ho, wo), "bf16")
+    mask = synth.bernoulli_mask(r, n, gh, gw, p) if p not in (0.0, 1.0) else np.full((n, gh, gw), int(p), np.uint8)
+    a = oracle.sparse_conv2d(x, wt, mask, prev, "bf16", s, pad, bias, rb, relu)
+    b = oracle.sparse_conv2d_active(x, wt, mask, prev, "bf16", s, pad, bias, rb, relu)
+    assert np.array_equal(a, b)
