@@ -8,6 +8,7 @@
 // value per block, the frame state copies the executed blocks of the RGB frame, and
 // the information gain streams the class scores of two score maps once (HBM bound).
 #include "bc_internal.h"
+#include "compact.h"
 
 namespace bc {
 namespace {
@@ -39,22 +40,18 @@ __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint3
 
 // ---------------------------------------------------------------- sampling + index
 
-constexpr int kIdxThreads = 1024;
-constexpr int kIdxWaves = kIdxThreads / 64;
-
 // One workgroup walks the grid in rounds of 1024 blocks: each thread draws its block's
-// decision, writes it to the mask, and the ballot / masked-popcount / wave-prefix
-// compaction writes the executed ids in ascending order (stable ranks, no sort).
-__global__ __launch_bounds__(kIdxThreads) void k_sample_index(
+// decision and writes it to the mask, and the stable ballot compaction of compact.h
+// writes the executed ids in ascending order (no sort).
+__global__ __launch_bounds__(kCompactThreads) void k_sample_index(
     const float *__restrict__ prob, int total, uint32_t f0, uint32_t f1, uint32_t s0,
     uint32_t s1, uint8_t *__restrict__ mask, int32_t *__restrict__ idx,
     int32_t *__restrict__ count)
 {
-    __shared__ int wave_total[kIdxWaves];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ int wave_total[kCompactWaves];
     int running = 0;
-    for (int base = 0; base < total; base += kIdxThreads) {
-        const int i = base + tid;
+    for (int base = 0; base < total; base += kCompactThreads) {
+        const int i = base + (int)threadIdx.x;
         bool act = false;
         if (i < total) {
             const uint32_t x = philox_word0((uint32_t)i, f0, f1, 0u, s0, s1);
@@ -62,23 +59,9 @@ __global__ __launch_bounds__(kIdxThreads) void k_sample_index(
             act = u < prob[i];                            // false for a NaN probability
             mask[i] = act ? 1 : 0;
         }
-        const unsigned long long b = __ballot(act);
-        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0));
-        if (lane == 0) wave_total[wave] = __popcll(b);
-        __syncthreads();
-        int before = 0, round_total = 0;
-#pragma unroll
-        for (int w = 0; w < kIdxWaves; ++w) {
-            const int t = wave_total[w];
-            before += (w < wave) ? t : 0;
-            round_total += t;
-        }
-        if (act) idx[running + before + rank] = i;
-        running += round_total;
-        __syncthreads();
+        running += compact_round(act, i, idx, running, wave_total);
     }
-    if (tid == 0) *count = running;
+    if (threadIdx.x == 0) *count = running;
 }
 
 // ---------------------------------------------------------------- frame state
@@ -434,7 +417,7 @@ __global__ __launch_bounds__(kRwThreads) void k_block_rewards(
 hipError_t launch_sample_index(const float *prob, int total, uint64_t seed, uint64_t frame,
                                uint8_t *mask, int32_t *idx, int32_t *count, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_sample_index, dim3(1), dim3(kIdxThreads), 0, s, prob, total,
+    hipLaunchKernelGGL(k_sample_index, dim3(1), dim3(kCompactThreads), 0, s, prob, total,
                        (uint32_t)frame, (uint32_t)(frame >> 32), (uint32_t)seed,
                        (uint32_t)(seed >> 32), mask, idx, count);
     return hipGetLastError();
