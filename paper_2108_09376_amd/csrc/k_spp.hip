@@ -10,7 +10,7 @@
 //     ran this frame, transferred elsewhere): per bin the mean of its pixels, a 1x1
 //     convolution (weights [level][cl][c]) plus bias, ReLU, one round to the storage
 //     format, written to the caller's level buffer [n][bins][cl] (k_spp_levels16,
-//     one workgroup per bin; about 0.5 MB read at 2048x1024);
+//     one 1024-thread workgroup per bin; about 0.5 MB read at 2048x1024);
 //  2. writes the executed output blocks of the concatenation [input, up(level 0),
 //     ..., up(level L-1)]: the input's own bits, then each level resampled bilinearly
 //     to the map (pixel centres aligned) and rounded (k_spp_concat16, one thread per
@@ -56,16 +56,24 @@ __device__ __forceinline__ void bin_range(int i, int rows, int h, int &lo, int &
     hi = ((i + 1) * h + rows - 1) / rows;
 }
 
-// Level l's bins per image start at first[l]; 256 threads = (256 / vpp) pixel lanes x
-// vpp channel vectors of 8 (vpp = c / 8 divides 256, checked on the host).
+// One workgroup of kLvThreads threads per bin: (kLvThreads / vpp) pixel lanes x vpp
+// channel vectors of 8 (vpp = c / 8 divides 256, so it divides kLvThreads; checked on
+// the host). A thread keeps kSppBatch loads in flight (offsets past the bin read zero)
+// and adds them in pixel order; the pixel lanes are then added pairwise in a fixed
+// tree. The 1x1 convolution splits each output channel's dot product over
+// kLvThreads / cl threads (channel ranges in order), their partial sums added in range
+// order: every sum has a fixed order, so results do not depend on the schedule.
+constexpr int kLvThreads = 1024;
+constexpr int kSppBatch = 8;
+
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void k_spp_levels16(const uint16_t *__restrict__ in,
-                                                            const uint16_t *__restrict__ w,
-                                                            const float *__restrict__ bias,
-                                                            uint16_t *__restrict__ levels,
-                                                            SppGeom g)
+__global__ __launch_bounds__(kLvThreads) void k_spp_levels16(const uint16_t *__restrict__ in,
+                                                              const uint16_t *__restrict__ w,
+                                                              const float *__restrict__ bias,
+                                                              uint16_t *__restrict__ levels,
+                                                              SppGeom g)
 {
-    __shared__ float part[kThreads][8];
+    __shared__ float part[kLvThreads][8];
     __shared__ float mean[kMaxSppChannels];
     const int tid = threadIdx.x;
     const int tb = g.first[g.levels];
@@ -78,48 +86,86 @@ __global__ __launch_bounds__(kThreads) void k_spp_levels16(const uint16_t *__res
     bin_range(bi, g.rows[l], g.h, r0, r1);
     bin_range(bj, g.cols[l], g.w, c0, c1);
     const int bw = c1 - c0, npix = (r1 - r0) * bw;
-    const int lanes = kThreads / g.vpp;
+    const int lanes = kLvThreads / g.vpp;
     const int lane = tid / g.vpp, v = tid - lane * g.vpp;
     const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
         (void *)in, (short)0, g.in_bytes, kBufferFlags);
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int p = lane; p < npix; p += lanes) {
-        const int y = r0 + p / bw, x = c0 + (p - (p / bw) * bw);
-        const i32x4 d = __builtin_amdgcn_raw_buffer_load_b128(
-            rin, ((((img * g.h + y) * g.w + x) * g.vpp) + v) * 16, 0, 0);
+    // the convolution's first batch of weights is requested with the pixels (it does not
+    // depend on them)
+    const int Q = kLvThreads / g.cl;
+    const int co = tid % g.cl, q = tid / g.cl;
+    const int v0 = q < Q ? (q * g.vpp) / Q : 0, v1 = q < Q ? ((q + 1) * g.vpp) / Q : 0;
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)w, (short)0, g.w_bytes, kBufferFlags);
+    const int row = (l * g.cl + co) * g.c * 2;           // bytes of weight row (l, co)
+    i32x4 wv[kSppBatch];
+    auto load_w = [&](int cv0, i32x4 (&r)[kSppBatch]) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            acc[2 * t] += h16_to_f32<BF16>((uint32_t)d[t] & 0xFFFFu);
-            acc[2 * t + 1] += h16_to_f32<BF16>((uint32_t)d[t] >> 16);
+        for (int u = 0; u < kSppBatch; ++u)
+            r[u] = __builtin_amdgcn_raw_buffer_load_b128(
+                rw, cv0 + u < v1 ? row + (cv0 + u) * 16 : kOutOfRange, 0, 0);
+    };
+    load_w(v0, wv);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int p0 = lane; p0 < npix; p0 += kSppBatch * lanes) {
+        i32x4 d[kSppBatch];
+#pragma unroll
+        for (int u = 0; u < kSppBatch; ++u) {
+            const int p = p0 + u * lanes;
+            const int y = r0 + p / bw, x = c0 + (p - (p / bw) * bw);
+            d[u] = __builtin_amdgcn_raw_buffer_load_b128(
+                rin, p < npix ? ((((img * g.h + y) * g.w + x) * g.vpp) + v) * 16 : kOutOfRange, 0, 0);
         }
+#pragma unroll
+        for (int u = 0; u < kSppBatch; ++u)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                acc[2 * t] += h16_to_f32<BF16>((uint32_t)d[u][t] & 0xFFFFu);
+                acc[2 * t + 1] += h16_to_f32<BF16>((uint32_t)d[u][t] >> 16);
+            }
     }
 #pragma unroll
     for (int t = 0; t < 8; ++t) part[tid][t] = acc[t];
     __syncthreads();
+    // pixel lanes pairwise: lane i takes lane i + half, halves shrinking (lanes is a
+    // power of two: kLvThreads and vpp are)
+    for (int half = lanes / 2; half >= 1; half /= 2) {
+        if (lane < half) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t) part[tid][t] += part[tid + half * g.vpp][t];
+        }
+        __syncthreads();
+    }
     if (tid < g.vpp) {
-        float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        for (int q = 0; q < lanes; ++q)                  // lanes in order: a fixed sum
 #pragma unroll
-            for (int t = 0; t < 8; ++t) s[t] += part[q * g.vpp + tid][t];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) mean[tid * 8 + t] = s[t] / (float)npix;
+        for (int t = 0; t < 8; ++t) mean[tid * 8 + t] = part[tid][t] / (float)npix;
     }
     __syncthreads();
-    if (tid < g.cl) {
-        const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)w, (short)0, g.w_bytes, kBufferFlags);
-        const int row = (l * g.cl + tid) * g.c * 2;      // bytes of weight row (l, tid)
-        float z = bias ? bias[l * g.cl + tid] : 0.f;
-        for (int cv = 0; cv < g.vpp; ++cv) {
-            const i32x4 d = __builtin_amdgcn_raw_buffer_load_b128(rw, row + cv * 16, 0, 0);
+    // 1x1 convolution: thread t = q * cl + co takes channel vectors [q vpp / Q, (q+1) vpp / Q)
+    // of output channel co (Q = kLvThreads / cl parts)
+    float z = 0.f;
+    if (q < Q) {
+        for (int cv0 = v0; cv0 < v1; cv0 += kSppBatch) {
+            if (cv0 > v0) load_w(cv0, wv);               // the first batch came in with the pixels
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                z += h16_to_f32<BF16>((uint32_t)d[t] & 0xFFFFu) * mean[cv * 8 + 2 * t];
-                z += h16_to_f32<BF16>((uint32_t)d[t] >> 16) * mean[cv * 8 + 2 * t + 1];
+            for (int u = 0; u < kSppBatch; ++u) {
+                if (cv0 + u >= v1) break;
+                const int cb = (cv0 + u) * 8;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    z += h16_to_f32<BF16>((uint32_t)wv[u][t] & 0xFFFFu) * mean[cb + 2 * t];
+                    z += h16_to_f32<BF16>((uint32_t)wv[u][t] >> 16) * mean[cb + 2 * t + 1];
+                }
             }
         }
-        z = (z > 0.f || z != z) ? z : 0.f;
-        levels[((size_t)img * tb + bin) * g.cl + tid] = (uint16_t)f32_to_h16<BF16>(z);
+    }
+    part[tid][1] = z;                                    // column 1: free since the tree
+    __syncthreads();
+    if (tid < g.cl) {
+        float zz = bias ? bias[l * g.cl + tid] : 0.f;
+        for (int qq = 0; qq < Q; ++qq) zz += part[qq * g.cl + tid][1];   // parts in order
+        zz = (zz > 0.f || zz != zz) ? zz : 0.f;
+        levels[((size_t)img * tb + bin) * g.cl + tid] = (uint16_t)f32_to_h16<BF16>(zz);
     }
 }
 
@@ -209,9 +255,9 @@ hipError_t launch_spp(const uint16_t *in, const uint16_t *w, const float *bias, 
 {
     const unsigned bins = (unsigned)g.n * g.first[g.levels];
     if (bf16)
-        hipLaunchKernelGGL(k_spp_levels16<true>, dim3(bins), dim3(kThreads), 0, s, in, w, bias, levels, g);
+        hipLaunchKernelGGL(k_spp_levels16<true>, dim3(bins), dim3(kLvThreads), 0, s, in, w, bias, levels, g);
     else
-        hipLaunchKernelGGL(k_spp_levels16<false>, dim3(bins), dim3(kThreads), 0, s, in, w, bias, levels, g);
+        hipLaunchKernelGGL(k_spp_levels16<false>, dim3(bins), dim3(kLvThreads), 0, s, in, w, bias, levels, g);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int nv = g.bh * g.bw * (g.cout / 8);
