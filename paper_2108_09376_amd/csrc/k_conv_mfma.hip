@@ -98,6 +98,7 @@ struct MfmaArgs {
     int ksplit, cps;                    // K slices per tile, 32-channel chunks per slice
     int tiles_full;                     // tiles (incl. K slices) of a full frame
     int slots;                          // stem form: workgroups resident on the device
+    int xu, gx;                         // XCD grouping of the tile order (xcd_tile), 0 = off
 };
 
 template <bool BF16>
@@ -782,10 +783,27 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
     epi.finish(a, acc, smem, n0);
 }
 
+// Tile order grouped by XCD. Workgroups go to the 8 XCDs in turn (workgroup b to XCD
+// b % 8), and each XCD has an L2 of its own. The R = ntn * ksplit workgroups of one M
+// tile read the same input rows; in plain order they land on every XCD, and each XCD
+// fetches those rows. Grouped, an M tile's workgroups form gx units of xu = R / gx
+// consecutive tiles; unit U = mt * gx + part runs on XCD U % 8, so the input rows of an
+// M tile are fetched by gx XCDs, and consecutive M tiles (the active ones come first)
+// still spread over all XCDs. Returns the natural tile index, or a value past the grid
+// for the padding workgroups (their tile is beyond the frame, and they exit).
+__device__ __forceinline__ int xcd_tile(const MfmaArgs &a, int b)
+{
+    if (!a.xu) return b;
+    const int j = b >> 3;
+    const int U = (b & 7) + 8 * (j / a.xu);
+    const int mt = U / a.gx, part = U - mt * a.gx;
+    return (mt * a.gx + part) * a.xu + (j - (j / a.xu) * a.xu);
+}
+
 template <bool BF16, int BM, int BN, int KS, int S, int SG>
 __global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
 {
-    conv_pipe_tile<BF16, BM, BN, KS, S, SG>(a, blockIdx.x);
+    conv_pipe_tile<BF16, BM, BN, KS, S, SG>(a, xcd_tile(a, blockIdx.x));
 }
 
 // Two independent 1x1 layers of one frame in one launch (a block's shortcut projection
@@ -1121,6 +1139,7 @@ int pipe_au(int BM, int KT, int S) { return KT == 1 ? BM / 64 : (BM == 64 ? (S =
 bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 {
     MfmaArgs &a = pl.a;
+    a.xu = a.gx = 0;
     if (g.cout % BN) return false;
     if (!tile_rows(g, BM, a)) return false;
     const int KS = g.kh, S = g.stride;
@@ -1241,6 +1260,19 @@ bool choose_plan(const LayerGeom &g, Plan &best)
                     best.sg = 2;
                     best.lds = lds;
                 }
+            }
+            // 1x1 layers whose M tiles have several workgroups: grouped by XCD (xcd_tile),
+            // units of at most 16 workgroups. The tile a workgroup computes, and so the
+            // result, does not change; only which XCD computes it.
+            best.a.xu = best.a.gx = 0;
+            const int R = a.ntn * a.ksplit;
+            if (g.kh == 1 && R >= 2) {
+                a.gx = (R + 15) / 16;
+                while (R % a.gx) ++a.gx;
+                a.xu = R / a.gx;
+                const unsigned mt_full = best.grid / (unsigned)R;
+                const unsigned units = mt_full * (unsigned)a.gx;
+                best.grid = ((units + 7) / 8) * 8 * (unsigned)a.xu;
             }
             best.a.tiles_full = (int)best.grid;
             return true;
@@ -1556,6 +1588,11 @@ hipError_t launch_conv_pair_nhwc_mfma(const ConvCall &c1, const ConvCall &c2, Ha
     fill_plan(c1.x, c1.w, c1.bias, c1.res, c1.y, c1.relu, c1.g, p1);
     fill_plan(c2.x, c2.w, c2.bias, c2.res, c2.y, c2.relu, c2.g, p2);
     const int v1 = pair_variant(p1), v2 = pair_variant(p2);
+    for (Plan *p : {&p1, &p2})                  // the paired launch keeps the plain tile order
+        if (p->a.xu) {
+            p->a.xu = p->a.gx = 0;
+            p->grid = p->tiles * (unsigned)p->a.ksplit;
+        }
     if (fmt == Half16::BF16 && c1.g.kh == 1 && c2.g.kh == 1 && c2.g.stride == 1 && v1 >= 0 &&
         v2 >= 0 && p1.grid > 0 && p2.grid > 0 && (size_t)p1.grid + p2.grid < (1u << 31) &&
         p1.lds < 60 * 1024 && p2.lds < 60 * 1024) {   // no dynamic-LDS opt-in needed
