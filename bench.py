@@ -61,8 +61,9 @@ def parse():
                     help="print the matrix-core / LDS counter table of a rocprofv3 --pmc run")
     ap.add_argument("--pmc-gather-scatter", action="store_true",
                     help="run only the standalone gather/scatter cases for a rocprofv3 --pmc run")
-    ap.add_argument("--gs-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="print the gather/scatter traffic table of two rocprofv3 --pmc runs")
+    ap.add_argument("--gs-summary", nargs="+", metavar="CSV",
+                    help="FETCH_CSV WRITE_CSV [KERNEL_TRACE_CSV]: print the gather/scatter traffic table "
+                         "of two rocprofv3 --pmc runs (and rates over the kernel durations of a trace run)")
     ap.add_argument("--cpu-configs", action="store_true",
                     help="time the CPU oracle on configurations 1, 2, 4 and 5 (both modes) and exit")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -577,9 +578,11 @@ def pmc_gather_scatter(torch, bc, dev, reps=3):
     torch.cuda.synchronize()
 
 
-def gs_summary(fetch_csv, write_csv):
+def gs_summary(fetch_csv, write_csv, trace_csv=None):
     """Text summary of the two counter runs of pmc_gather_scatter: calibrated FETCH and
-    WRITE bytes per gather / scatter dispatch against the algorithmic bytes."""
+    WRITE bytes per gather / scatter dispatch against the algorithmic bytes; with the
+    kernel trace of a third run of the same command, each op's median kernel duration
+    and the counters' bytes over it (GB/s and fraction of the 8 TB/s HBM peak)."""
     import csv
     res = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
@@ -608,6 +611,20 @@ def gs_summary(fetch_csv, write_csv):
             out.append(f"{op + '_' + tag:26s} {f / 1e6:9.3f} {w / 1e6:9.3f} {(f + w) / 1e6:9.3f} "
                        f"{algo[op] / 1e6:9.3f} {(f + w) / algo[op]:6.2f}")
             kv.append(f"hbm_bytes_{op}_{tag}={f + w:.0f}")
+    if trace_csv:
+        tr = [r for r in csv.DictReader(open(trace_csv))
+              if "k_gather_" in r["Kernel_Name"] or "k_scatter_" in r["Kernel_Name"]]
+        tr.sort(key=lambda r: int(r["Start_Timestamp"]))
+        out.append("kernel durations (trace run, each op after a 512 MiB cache-evicting read; median of "
+                   f"{len(tr) // 6} rounds) and counter bytes over them:")
+        for k, (tag, c, allb) in enumerate(GS_CASES):
+            for j, op in enumerate(("gather", "scatter")):
+                ds = sorted((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                            for r in tr[2 * k + j::6])
+                us = ds[len(ds) // 2]
+                hb = float(dict(x.split("=") for x in kv)[f"hbm_bytes_{op}_{tag}"])
+                out.append(f"  {op + '_' + tag:26s} {us:7.2f} us  {hb / us / 1e3:8.1f} GB/s  "
+                           f"{hb / us / 1e3 / PEAK_HBM_GBS:5.3f} of HBM peak")
     out += kv
     out.append(f"gs_source_sha256={gs_source_sha()}")
     return "\n".join(out)
