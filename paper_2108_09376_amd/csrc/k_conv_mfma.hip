@@ -99,6 +99,7 @@ struct MfmaArgs {
     int tiles_full;                     // tiles (incl. K slices) of a full frame
     int slots;                          // stem form: workgroups resident on the device
     int xu, gx;                         // XCD grouping of the tile order (xcd_tile), 0 = off
+    int grp_lds;                        // pipelined form: LDS bytes of one wave group
 };
 
 template <bool BF16>
@@ -196,7 +197,8 @@ __device__ __forceinline__ bool load_tile_blocks(const MfmaArgs &a, int mt, Tile
 // output this lane will write, so those round trips overlap the K loop. finish() transposes the fp32 accumulators through LDS (each lane then owns 8
 // consecutive channels of one pixel), adds bias and residual, applies ReLU, rounds to
 // the storage format and writes with 16-byte buffer stores; rows of inactive patches
-// use an out-of-range offset, which the hardware drops.
+// use an out-of-range offset, which the hardware drops. `tid` is the thread's index in
+// its group of four waves; a group that is not `live` only takes the barriers.
 template <bool BF16, int BM, int BN>
 struct Epilogue {
     static constexpr int WM = BM / 2, WN = BN / 2, MI = WM / 16;
@@ -205,9 +207,10 @@ struct Epilogue {
     uint4 res[NP][NU];
     uint4 bias[NP][2];         // bias of this lane's 8 output channels per pass (fp32 bits)
 
-    __device__ __forceinline__ void prefetch(const MfmaArgs &a, const TileBlocks &tb, int n0)
+    __device__ __forceinline__ void prefetch(const MfmaArgs &a, const TileBlocks &tb, int n0,
+                                             int tid = threadIdx.x)
     {
-        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int lane = tid & 63, wave = tid >> 6;
         const int wm = wave >> 1, wn = wave & 1;
         // no bias: an empty buffer, every load returns zeros
         const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
@@ -244,9 +247,10 @@ struct Epilogue {
     }
 
     __device__ __forceinline__ void finish(const MfmaArgs &a, f32x4 (&acc)[BM / 32][BN / 32],
-                                           uint8_t *smem, int n0)
+                                           uint8_t *smem, int n0, int tid = threadIdx.x,
+                                           bool live = true)
     {
-        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int lane = tid & 63, wave = tid >> 6;
         const int wn = wave & 1;
         float *scr = (float *)smem + wave * (WM * EPITCH);
         const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
@@ -254,15 +258,18 @@ struct Epilogue {
 #pragma unroll
         for (int np = 0; np < NP; ++np) {
             __syncthreads();
+            if (live) {
 #pragma unroll
-            for (int mi = 0; mi < MI; ++mi)
+                for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-                for (int nn = 0; nn < 2; ++nn)
+                    for (int nn = 0; nn < 2; ++nn)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        scr[(mi * 16 + 4 * (lane >> 4) + i) * EPITCH + nn * 16 + (lane & 15)] =
-                            acc[mi][np * 2 + nn][i];
+                        for (int i = 0; i < 4; ++i)
+                            scr[(mi * 16 + 4 * (lane >> 4) + i) * EPITCH + nn * 16 + (lane & 15)] =
+                                acc[mi][np * 2 + nn][i];
+            }
             __syncthreads();
+            if (!live) continue;
             const int cl = wn * WN + np * 32 + (lane & 3) * 8;   // column within the tile
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
@@ -569,7 +576,12 @@ __device__ __forceinline__ void ring_loop(F &f, int n)
 // SG (stage grouping) sets how much of K one barrier covers: one tap (SG = 1), all KT
 // taps of a 32-channel chunk (SG = KT, 3x3 layers), or two chunks (SG = 2, 1x1 layers).
 // One workgroup's tile L of the launch grid (the kernels below give it blockIdx.x).
-template <bool BF16, int BM, int BN, int KS, int S, int SG>
+// WGS groups of four waves split the tile's K slice in two contiguous halves (the
+// first group takes the first half); each group runs the same number of steps (a
+// shorter second half walks zeros at the end), and the second group's partial sums
+// are added to the first's through LDS before the epilogue: eight waves per tile raise
+// the LDS read rate of the few-tile layers whose workgroups do not fill the CUs.
+template <bool BF16, int BM, int BN, int KS, int S, int SG, int WGS = 1>
 __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
 {
     constexpr int SS = (KS == 1) ? S : 1;
@@ -583,7 +595,8 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
     __shared__ TileBlocks tb;
     __shared__ int s_last;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = (WGS == 1) ? 0 : (int)(threadIdx.x >> 8);
+    const int tid = threadIdx.x & (kThreads - 1), lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1, q = tid & 3;
     // natural tile order L = (mt * ntn + nt) * ksplit + ks: N tile and K slice are known
     // without the active count
@@ -593,9 +606,12 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
     const int mt = mn / a.ntn;
     const int n0 = nt * BN;
     const int nchunk = (a.cin + BK - 1) / BK;
-    const int c_lo = ks * a.cps;
-    const int c_hi = min(nchunk, c_lo + a.cps);
-    const int nsteps = (c_hi - c_lo) * KT;
+    const int s_lo = ks * a.cps, s_hi = min(nchunk, s_lo + a.cps);
+    const int half = (s_hi - s_lo + WGS - 1) / WGS;      // chunks per group (the trip count)
+    const int c_lo = s_lo + grp * half;
+    const int c_hi = min(s_hi, c_lo + half);
+    const int nsteps = (c_hi > c_lo ? c_hi - c_lo : 0) * KT;   // this group's real steps
+    const int nstrip = half * KT;                         // steps every group runs
 
     // Every request is issued unconditionally as a raw buffer load: lanes without data
     // (zero padding, inactive patches, channels past Cin, steps past the slice) use an
@@ -619,8 +635,8 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
     constexpr int AG = (KT == 1) ? SG : 1;        // halo chunks per stage buffer
     const int hrhc = a.HR * a.HC;
     const int aslot = ((a.nslot + 15) & ~15) * PITCH;
-    uint8_t *sA = smem;
-    uint8_t *sB = smem + 2 * AG * aslot;
+    uint8_t *sA = smem + grp * a.grp_lds;
+    uint8_t *sB = sA + 2 * AG * aslot;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)a.x, (short)0, a.x_bytes, kBufferFlags);
 
@@ -706,7 +722,7 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
         };
 #pragma unroll
         for (int d = 0; d < D; ++d) load_stage(d, ra[d], rb[d]);
-        epi.prefetch(a, tb, n0);
+        if (grp == 0) epi.prefetch(a, tb, n0, tid);
         auto step = [&](auto dc, int st) {
             constexpr int d = decltype(dc)::value;
             uint8_t *sa = sA + (st & 1) * SG * aslot;
@@ -721,7 +737,7 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
 #pragma unroll
             for (int g = 0; g < SG; ++g) compute(sa + g * aslot, sb + g * BN * PITCH, 0);
         };
-        ring_loop<D>(step, (nsteps + SG - 1) / SG);
+        ring_loop<D>(step, (nstrip + SG - 1) / SG);
     } else if constexpr (SG == 1) {
         // one chunk = KT steps: the next chunk's weights (all taps) and halo are requested
         // while the current chunk is multiplied
@@ -730,8 +746,8 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
         load_a(c_lo, ra);
 #pragma unroll
         for (int t = 0; t < KT; ++t) load_b(t, rb[t]);
-        epi.prefetch(a, tb, n0);
-        const int nch = c_hi - c_lo;
+        if (grp == 0) epi.prefetch(a, tb, n0, tid);
+        const int nch = nstrip / KT;
         for (int cj = 0; cj < nch; ++cj) {
             uint8_t *sa = sA + (cj & 1) * aslot;
             store_a(sa, ra);
@@ -751,7 +767,7 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
         // staged under one barrier; chunks ride a 2-deep register ring and an LDS double
         // buffer (sB holds KT slices per buffer)
         constexpr int D = 2;
-        const int nch = c_hi - c_lo;
+        const int nch = nstrip / KT;
         uint4 ra[D][AU];
         uint4 rb[D][KT][BV];
         auto load_stage = [&](int cj, uint4 (&xa)[AU], uint4 (&xb)[KT][BV]) {
@@ -761,7 +777,7 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
         };
 #pragma unroll
         for (int d = 0; d < D; ++d) load_stage(d, ra[d], rb[d]);
-        epi.prefetch(a, tb, n0);
+        if (grp == 0) epi.prefetch(a, tb, n0, tid);
         auto step = [&](auto dc, int cj) {
             constexpr int d = decltype(dc)::value;
             uint8_t *sa = sA + (cj & 1) * aslot;
@@ -778,9 +794,28 @@ __device__ __forceinline__ void conv_pipe_tile(const MfmaArgs &a, const int L)
         ring_loop<D>(step, nch);
     }
 
-    if constexpr (BM == 64 && BN == 64)
+    if constexpr (WGS == 2) {
+        // the second group's partial sums join the first's (first + second, per element)
+        __syncthreads();                  // both groups are done with their stage buffers
+        f32x4 *red = (f32x4 *)smem + (wave * MI * NI) * 64 + lane;
+        if (grp == 1) {
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) red[(mi * NI + ni) * 64] = acc[mi][ni];
+        }
+        __syncthreads();
+        if (grp == 0) {
+#pragma unroll
+            for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = acc[mi][ni] + red[(mi * NI + ni) * 64];
+        }
+        __syncthreads();                  // the epilogue scratch reuses the same LDS
+    }
+    if constexpr (BM == 64 && BN == 64 && WGS == 1)
         if (a.ksplit > 1 && !split_k_handoff(a, acc, mt * a.ntn + nt, ks, &s_last)) return;
-    epi.finish(a, acc, smem, n0);
+    epi.finish(a, acc, smem, n0, tid, grp == 0);
 }
 
 // Tile order grouped by XCD. Workgroups go to the 8 XCDs in turn (workgroup b to XCD
@@ -800,10 +835,10 @@ __device__ __forceinline__ int xcd_tile(const MfmaArgs &a, int b)
     return (mt * a.gx + part) * a.xu + (j - (j / a.xu) * a.xu);
 }
 
-template <bool BF16, int BM, int BN, int KS, int S, int SG>
-__global__ __launch_bounds__(kThreads) void k_conv_pipe(MfmaArgs a)
+template <bool BF16, int BM, int BN, int KS, int S, int SG, int WGS = 1>
+__global__ __launch_bounds__(kThreads * WGS) void k_conv_pipe(MfmaArgs a)
 {
-    conv_pipe_tile<BF16, BM, BN, KS, S, SG>(a, xcd_tile(a, blockIdx.x));
+    conv_pipe_tile<BF16, BM, BN, KS, S, SG, WGS>(a, xcd_tile(a, blockIdx.x));
 }
 
 // Two independent 1x1 layers of one frame in one launch (a block's shortcut projection
@@ -1082,6 +1117,7 @@ struct Plan {
     Form form;
     MfmaArgs a;
     int sg = 1;                // pipelined form: stage grouping (k_conv_pipe's SG)
+    int wgs = 1;               // pipelined form: groups of four waves per tile (K halves)
     unsigned tiles;            // output tiles of a full frame (before any K split)
     size_t lds;
     size_t ws_bytes;
@@ -1140,6 +1176,8 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 {
     MfmaArgs &a = pl.a;
     a.xu = a.gx = 0;
+    a.grp_lds = 0;
+    pl.wgs = 1;
     if (g.cout % BN) return false;
     if (!tile_rows(g, BM, a)) return false;
     const int KS = g.kh, S = g.stride;
@@ -1260,6 +1298,16 @@ bool choose_plan(const LayerGeom &g, Plan &best)
                     best.sg = 2;
                     best.lds = lds;
                 }
+            }
+            // 1x1 layers with a long K on few tiles (stride-16 1024 -> 256): two groups of
+            // four waves per tile, each taking half of K; the workgroups do not fill the
+            // CUs there, and eight waves per CU read LDS faster than four
+            if (g.kh == 1 && best.BM == 64 && best.BN == 64 && best.sg == 2 && a.ksplit == 1 &&
+                nchunk >= 16 && tiles <= 512) {
+                const size_t main = pipe_lds(a.nslot, 64, 64, 2, 1);
+                a.grp_lds = (int)main;
+                best.wgs = 2;
+                best.lds = 2 * main;
             }
             // 1x1 layers whose M tiles have several workgroups: grouped by XCD (xcd_tile),
             // units of at most 16 workgroups. The tile a workgroup computes, and so the
@@ -1391,7 +1439,7 @@ hipError_t launch_kernel(K kernel, const Plan &p, hipStream_t s)
             g_attr_lds[i].lds = p.lds;
         }
     }
-    hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads), p.lds, s, p.a);
+    hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(kThreads * p.wgs), p.lds, s, p.a);
     return hipSuccess;
 }
 
@@ -1408,8 +1456,10 @@ hipError_t launch_one(const Plan &p, hipStream_t s)
             // all-tap stages exist for the 64x64 tiles the planner gives them to
                 if constexpr (BM == 64 && BN == 64 && KS == 3)
                 if (p.sg == 9) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 9>, p, s);
-            if constexpr (BM == 64 && BN == 64 && KS == 1)
+            if constexpr (BM == 64 && BN == 64 && KS == 1) {
+                if (p.sg == 2 && p.wgs == 2) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 2, 2>, p, s);
                 if (p.sg == 2) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 2>, p, s);
+            }
             if (p.sg == 1) return launch_kernel(k_conv_pipe<BF16, BM, BN, KS, S, 1>, p, s);
         }
     } else {
@@ -1529,7 +1579,7 @@ hipError_t launch_plan(Plan &p, Half16 fmt, const LayerGeom &g, hipStream_t s, c
 // two chunks per barrier; 1 = 128 wide, one chunk; -1 = another form.
 int pair_variant(const Plan &p)
 {
-    if (p.form != Form::Pipe || p.BM != 64 || p.a.ksplit != 1) return -1;
+    if (p.form != Form::Pipe || p.BM != 64 || p.a.ksplit != 1 || p.wgs != 1) return -1;
     if (p.BN == 64 && p.sg == 2) return 0;
     if (p.BN == 128 && p.sg == 1) return 1;
     return -1;

@@ -172,6 +172,10 @@ CASES = [
                                                         # in three (11, 11, 10 chunks)
     (256, 128, 64, 128, 8, 16, 3, 1, True, True, 0.3),  # 3x3, 8 chunks on 256 tiles: K split in
                                                         # two, nine-tap stages
+    (520, 64, 16, 32, 2, 4, 1, 1, True, True, 0.5),     # 1x1, 17 chunks on few tiles: K halves
+                                                        # over two wave groups (9 and 8 chunks)
+    (744, 128, 16, 32, 2, 4, 1, 1, False, False, 0.6),  # 1x1, 24 chunks, the last a quarter
+                                                        # full, two wave groups
 ]
 
 
