@@ -217,7 +217,7 @@ def logit_grad(reward, mask, prob):
     return -np.asarray(reward, np.float64) * (a - np.asarray(prob, np.float64))
 
 
-def policy_backward(table, weights, biases, x, dz, stored=None):
+def policy_backward(table, weights, biases, x, dz, stored=None, return_maps=False):
     """Gradients of L with respect to every layer's weights and bias, float64.
 
     weights[l]: [cout, cin, k, k] (OIHW), biases[l]: [cout], x: S_t [n, 32, h, w] values,
@@ -229,10 +229,10 @@ def policy_backward(table, weights, biases, x, dz, stored=None):
     correlation of the layer's input with the output gradient), the bias gradient (its
     sum) and the input gradient (the transposed convolution), added to every producer
     that the layer reads (its source, and its residual source as is). torch's conv
-    primitives in float64 are the steps. Returns (dW list, db list)."""
+    primitives in float64 are the steps (layer_backward). Returns (dW list, db list), and
+    with return_maps also each layer's gated output gradient (the gp of layer_backward)."""
     import torch
     import torch.nn.functional as F
-    from torch.nn.grad import conv2d_input, conv2d_weight
     t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
     xs = t(x)
     ys = []
@@ -248,19 +248,35 @@ def policy_backward(table, weights, biases, x, dz, stored=None):
     g = [torch.zeros_like(y) for y in ys]
     g[-1][:, 0] = t(dz)
     dw, db = [None] * len(table), [None] * len(table)
+    gps = [None] * len(table)
     for li in range(len(table) - 1, -1, -1):
         l = table[li]
         gp = g[li] * (ys[li] > 0) if l["relu"] else g[li]
+        gps[li] = gp.numpy()
         src = xs if l["src"] < 0 else ys[l["src"]]
-        dw[li] = conv2d_weight(src, t(weights[li]).shape, gp, stride=l["stride"],
-                               padding=l["pad"]).numpy()
-        db[li] = gp.sum(dim=(0, 2, 3)).numpy()
+        dw[li], db[li], dx = layer_backward(l, weights[li], src.numpy(), gp.numpy())
         if l["src"] >= 0:
-            g[l["src"]] += conv2d_input(src.shape, t(weights[li]), gp, stride=l["stride"],
-                                        padding=l["pad"])
+            g[l["src"]] += t(dx)
         if l["res"] is not None:
             g[l["res"]] += gp
+    if return_maps:
+        return dw, db, gps
     return dw, db
+
+
+def layer_backward(layer, weight, src, gp):
+    """One layer's step of the reverse pass, float64: the weight gradient (the correlation
+    of the layer's input `src` with its output gradient `gp`, taken after the ReLU gate),
+    the bias gradient (the sum of gp over images and pixels) and the input gradient (the
+    transposed convolution of gp with the layer's weights). Returns (dW, db, dX)."""
+    import torch
+    from torch.nn.grad import conv2d_input, conv2d_weight
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    src, gp, w = t(src), t(gp), t(weight)
+    dw = conv2d_weight(src, w.shape, gp, stride=layer["stride"], padding=layer["pad"]).numpy()
+    db = gp.sum(dim=(0, 2, 3)).numpy()
+    dx = conv2d_input(src.shape, w, gp, stride=layer["stride"], padding=layer["pad"]).numpy()
+    return dw, db, dx
 
 
 def rmsprop_step(w, v, grad, lr=1e-4, alpha=0.99, eps=1e-8, weight_decay=1e-3):

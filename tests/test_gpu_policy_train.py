@@ -11,6 +11,10 @@ oracle's reverse pass is pinned by finite differences) through the C ABI.
   reverse pass then carries into every earlier layer. Against an unrounded fp64
   forward pass the difference reaches 9 % at the stem, all of it from the activations'
   bf16 storage.
+* Every layer's reverse-pass primitives at the network's shapes, fed the oracle's own
+  stored activations and bf16-rounded output gradients, element by element against the
+  oracle's layer step within the float32 summation bound (teacher-forced: the per-layer
+  gate behind the end-to-end one).
 * The primitives (input gradient, weight and bias gradients, combine) against torch's
   float64 gradient routines on the same bf16 values, elementwise or norm-wise.
 * The RMSprop step element by element."""
@@ -70,6 +74,64 @@ def test_policy_gradients_match_oracle(R):
     for row in rows:
         print("  %2d %-22s %.2e %.2e" % row)
     assert max(max(e[2], e[3]) for e in rows) <= 5e-2
+
+
+def test_policy_backward_layers_teacher_forced(R):
+    """Every layer's reverse-pass primitives at the policy network's shapes (256x512
+    frame), fed the oracle's own stored forward activations and the oracle's gated output
+    gradient rounded to bf16 (the device keeps gradient maps in bf16), against the
+    oracle's layer step on the same values, element by element. The bound is the
+    worst case of a float32 sum of N terms in any order, N u sum |terms| (u = 2^-24:
+    products of bf16 values are exact in float32), for the weight and bias gradients,
+    plus one bf16 rounding (2^-8 relative) for the input gradient. No GPU value is fed to
+    the oracle."""
+    bc, _ = R
+    h, w, classes = 256, 512, 19
+    r = synth.rng(510)
+    fr = synth.to_storage_bits(synth.normal(r, (1, 3, h, w)), "bf16")
+    st = synth.to_storage_bits(synth.normal(r, (1, 3, h, w)), "bf16")
+    sc = synth.to_storage_bits(synth.normal(r, (1, 64, h // 4, w // 4), 3.0), "bf16")
+    m_prev = synth.bernoulli_mask(r, 1, 2, 4, 0.5)
+    reward = r.normal(0, 1, (1, 2, 4)).astype(np.float32)
+    act = synth.bernoulli_mask(r, 1, 2, 4, 0.5)
+    prob = r.uniform(0.05, 0.95, (1, 2, 4)).astype(np.float32)
+    table = onet.policy_table()
+    folded = onet.fold_params(table, onet.make_params(table, seed0=3100), "bf16")
+    ws = [oracle.value(f["w_bits"], "bf16") for f in folded]
+    bs = [f["bias"].astype(np.float64) for f in folded]
+    s_t = P.policy_input(fr, st, sc, classes, m_prev)
+    stored_bits = onet.dense_frame(table, folded, s_t, "bf16")
+    stored = [oracle.value(a, "bf16") for a in stored_bits]
+    _, _, gps = P.policy_backward(table, ws, bs, oracle.value(s_t, "bf16"),
+                                  P.logit_grad(reward, act, prob), stored=stored, return_maps=True)
+    u = 2.0 ** -24
+    for li, l in enumerate(table):
+        k, s_, pad = l["k"], l["stride"], l["pad"]
+        src_bits = s_t if l["src"] < 0 else stored_bits[l["src"]]
+        gp_bits = oracle.store(gps[li], "bf16")
+        src, gp = oracle.value(src_bits, "bf16"), oracle.value(gp_bits, "bf16")
+        want_dw, want_db, want_dx = P.layer_backward(l, ws[li], src, gp)
+        abs_dw, abs_db, abs_dx = P.layer_backward(l, np.abs(ws[li]), np.abs(src), np.abs(gp))
+        n_w = gp.shape[0] * gp.shape[2] * gp.shape[3]            # terms per weight element
+        dw = torch.zeros((l["cout"], k, k, l["cin"]), dtype=torch.float32, device="cuda")
+        db = torch.zeros(l["cout"], dtype=torch.float32, device="cuda")
+        bc.bc_conv2d_weight_grad((k, k, s_, pad, 0), _nhwc(src_bits), _nhwc(gp_bits), dw, db)
+        got_dw = dw.cpu().numpy().astype(np.float64).transpose(0, 3, 1, 2)
+        got_db = db.cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(got_dw - want_dw) <= 1.01 * n_w * u * abs_dw + 1e-37), l["name"]
+        assert np.all(np.abs(got_db - want_db) <= 1.01 * n_w * u * abs_db + 1e-37), l["name"]
+        if l["src"] < 0:
+            continue                                             # S_t takes no gradient
+        wdev = torch.from_numpy(np.ascontiguousarray(folded[li]["w_bits"].transpose(0, 2, 3, 1))
+                                .view(np.int16)).view(torch.bfloat16).cuda()
+        acc = np.zeros_like(src_bits)
+        out = torch.empty((src.shape[0], src.shape[2], src.shape[3], src.shape[1]),
+                          dtype=torch.bfloat16, device="cuda")
+        bc.bc_conv2d_input_grad((k, k, s_, pad, 0), _nhwc(gp_bits), wdev, _nhwc(acc), out)
+        got_dx = oracle.value(from_dev(out), "bf16")
+        n_x = l["cout"] * k * k                                  # terms per input element, at most
+        tol = 2.0 ** -8 * np.abs(want_dx) + 1.01 * (1 + 2.0 ** -8) * n_x * u * abs_dx + 1e-37
+        assert np.all(np.abs(got_dx - want_dx) <= tol), l["name"]
 
 
 def test_rmsprop_step_matches_oracle(R):
