@@ -527,11 +527,8 @@ GS_SOURCES = ("paper_2108_09376_amd/csrc/k_gather_scatter.hip",)
 
 
 def gs_source_sha():
-    import hashlib
-    h = hashlib.sha256()
-    for f in GS_SOURCES:
-        h.update(open(os.path.join(ROOT, f), "rb").read())
-    return h.hexdigest()[:16]
+    """Hash of the gather/scatter kernel code (code_sha)."""
+    return code_sha(GS_SOURCES)
 
 
 def gs_algo_bytes(c, all_blocks, n_act=38):
@@ -901,13 +898,23 @@ MFMA_PROFILE = os.path.join(ROOT, "profiles", "sparse_conv_mfma_lds_resnet50_204
 CONV_SOURCES = ("paper_2108_09376_amd/csrc/k_conv_mfma.hip", "paper_2108_09376_amd/csrc/bc_internal.h")
 
 
-def conv_source_sha():
-    """SHA-256 over the sparse-conv kernel sources: counters taken on other code are stale."""
+def code_sha(files):
+    """SHA-256 over the code of C/C++/HIP sources: comments and blank lines are removed,
+    so a change of wording leaves it alone and any change of code moves it."""
     import hashlib
+    import re
     h = hashlib.sha256()
-    for f in CONV_SOURCES:
-        h.update(open(os.path.join(ROOT, f), "rb").read())
+    for f in files:
+        t = open(os.path.join(ROOT, f)).read()
+        t = re.sub(r"/\*.*?\*/", "", t, flags=re.S)
+        t = re.sub(r"//[^\n]*", "", t)
+        h.update("\n".join(l.rstrip() for l in t.splitlines() if l.strip()).encode())
     return h.hexdigest()[:16]
+
+
+def conv_source_sha():
+    """Hash of the sparse-conv kernel code: counters taken on other code are stale."""
+    return code_sha(CONV_SOURCES)
 
 
 def pmc_summary(fetch_csv, write_csv):

@@ -446,9 +446,13 @@ __global__ __launch_bounds__(kThreads) void k_conv_mfma(MfmaArgs a)
 //    stores its fp32 partial tile, and the last slice to finish (a per-tile counter)
 //    adds the partials in fixed slice order 0, 1, ... and runs the epilogue, so the
 //    result does not depend on arrival order. The counter is reset by that last
-//    workgroup, so no memset is needed between calls (safe under graph replay).
+//    workgroup, so no memset is needed between calls (safe under graph replay);
+//  * splits K over two groups of four waves inside one workgroup for 1x1 layers with
+//    a long K on few tiles (conv_pipe_tile's WGS): eight waves per CU read LDS faster
+//    than four where the workgroups do not fill the CUs.
 // The summation order over K (chunk by chunk, taps in order) is the same for every
-// stage grouping, so the grouping never changes results.
+// stage grouping, so the grouping never changes results; the K splits fix their own
+// order (slices, then the halves of a wave-group split, added in order).
 
 constexpr int kMaxSplitTiles = 1 << 16;
 constexpr int kMaxSplit = 4;        // K slices per tile
@@ -1246,7 +1250,9 @@ bool make_plan(const LayerGeom &g, int BM, int BN, Plan &pl)
 // no cost at 50 or 100 %) and not below (SwiftNet's decoder laterals with 8 and 16
 // chunks: 7.3 -> 5.3 and 7.2 -> 6.6 us unsplit); three slices of the nine-tap 3x3
 // layers gain at 10-30 % but lose 2 % at 50-100 %, where their workgroups outnumber
-// the CUs.
+// the CUs. 1x1 layers with >= 16 chunks on at most 512 tiles that keep K whole take
+// two wave groups per tile (the stride-16 1024 -> 256 layers: 8.6 -> 7.7 us with one
+// active block, 9.1 -> 8.4 us with 38; frames -0.7 % at 30 %, +1.5 % with every block).
 // Other forms take the largest tile with >= 2048 workgroups on a full frame. The choice
 // depends on the layer's shape only, never on the active count, so an active block's
 // result does not depend on which other blocks are active.
