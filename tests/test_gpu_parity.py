@@ -176,6 +176,8 @@ CASES = [
                                                         # over two wave groups (9 and 8 chunks)
     (744, 128, 16, 32, 2, 4, 1, 1, False, False, 0.6),  # 1x1, 24 chunks, the last a quarter
                                                         # full, two wave groups
+    (512, 64, 32, 64, 2, 4, 1, 2, True, True, 0.5),     # 1x1/2, 16 chunks on few tiles: two
+                                                        # wave groups at stride 2
 ]
 
 
