@@ -37,13 +37,17 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_nhwc16(const uint16_t *__r
 {
     const int k = blockIdx.x / parts;
     const int part = blockIdx.x - k * parts;
+    // the block id is read with the active count, in one round trip (the index holds
+    // total_blocks entries, so the read is valid whether or not block k is active)
+    const int bid = g.idx ? g.idx[k] : k;
     const int cnt = g.count ? *g.count : g.total_blocks;
     if (k >= cnt) return;
     const int cv = g.cout / 8;
     const int e = part * kThreads + threadIdx.x;
     if (e >= g.bh * g.bw * cv) return;
-    int img, gy, gx;
-    block_of(g, k, img, gy, gx);
+    const int img = bid / (g.gh * g.gw);
+    const int rem = bid - img * g.gh * g.gw;
+    const int gy = rem / g.gw, gx = rem - gy * g.gw;
     const int p = e / cv, c8 = e - p * cv;
     const int py = p / g.bw, px = p - py * g.bw;
     const int oy = gy * g.bh + py, ox = gx * g.bw + px;
