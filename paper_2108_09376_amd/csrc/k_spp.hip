@@ -190,9 +190,10 @@ __global__ __launch_bounds__(kThreads) void k_spp_concat16(const uint16_t *__res
 {
     const int k = blockIdx.x / chunks;
     const int chunk = blockIdx.x - k * chunks;
+    // the block id with the active count, one round trip (k < total_blocks: a valid read)
+    const int bid = idx ? idx[k] : k;
     const int cnt = count ? *count : g.total_blocks;
     if (k >= cnt) return;
-    const int bid = idx ? idx[k] : k;
     const int img = bid / (g.gh * g.gw);
     const int rem = bid - img * g.gh * g.gw;
     const int gy = rem / g.gw, gx = rem - gy * g.gw;
