@@ -539,7 +539,7 @@ def gs_algo_bytes(c, all_blocks, n_act=38):
 def pmc_gather_scatter(torch, bc, dev, reps=3):
     """Counter runs of the standalone gather and scatter (rocprofv3 --pmc FETCH_SIZE,
     then WRITE_SIZE): the calibration negation (256 MiB read, 256 MiB written), then
-    `reps` rounds of gather / scatter on the tensors of gather_scatter() for C = 64,
+    `reps` repetitions of gather / scatter on the tensors of gather_scatter() for C = 64,
     C = 256 and C = 256 with every block, each op after a 512 MiB cache-evicting read."""
     import synth
     mask = synth.frac_mask(synth.SEED_MASK0, 8, 16, 0.3)
@@ -594,7 +594,7 @@ def gs_summary(fetch_csv, write_csv, trace_csv=None):
         factor = (256 << 10) / cal[-1]
         ops = [v * factor * 1024 for n, v in seq if "k_gather_" in n or "k_scatter_" in n]
         if len(ops) % 6:
-            raise SystemExit(f"{path}: {len(ops)} gather/scatter dispatches is not a whole number of rounds")
+            raise SystemExit(f"{path}: {len(ops)} gather/scatter dispatches is not a whole number of repetitions")
         res[counter] = (factor, [ops[i:i + 6] for i in range(0, len(ops), 6)])
     out = [f"calibration factors: FETCH_SIZE {res['FETCH_SIZE'][0]:.4f}, WRITE_SIZE {res['WRITE_SIZE'][0]:.4f}",
            f"{'op':26s} {'fetch_MB':>9s} {'write_MB':>9s} {'hbm_MB':>9s} {'algo_MB':>9s} {'ratio':>6s}"]
@@ -613,7 +613,7 @@ def gs_summary(fetch_csv, write_csv, trace_csv=None):
               if "k_gather_" in r["Kernel_Name"] or "k_scatter_" in r["Kernel_Name"]]
         tr.sort(key=lambda r: int(r["Start_Timestamp"]))
         out.append("kernel durations (trace run, each op after a 512 MiB cache-evicting read; median of "
-                   f"{len(tr) // 6} rounds) and counter bytes over them:")
+                   f"{len(tr) // 6} repetitions) and counter bytes over them:")
         for k, (tag, c, allb) in enumerate(GS_CASES):
             for j, op in enumerate(("gather", "scatter")):
                 ds = sorted((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
