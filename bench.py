@@ -59,6 +59,10 @@ def parse():
                     help="run only N plain steps (for rocprofv3) and print nothing else")
     ap.add_argument("--counter-summary", nargs=2, metavar=("COUNTER_CSV", "AGENT_CSV"),
                     help="print the matrix-core / LDS counter table of a rocprofv3 --pmc run")
+    ap.add_argument("--pmc-layers", type=int, default=0,
+                    help="run only the single-layer sweep, each layer 1 + N times, for a rocprofv3 --pmc run")
+    ap.add_argument("--layer-counter-summary", nargs=2, metavar=("COUNTER_CSV", "AGENT_CSV"),
+                    help="print the matrix-core / LDS counter table of a --pmc-layers run")
     ap.add_argument("--pmc-gather-scatter", action="store_true",
                     help="run only the standalone gather/scatter cases for a rocprofv3 --pmc run")
     ap.add_argument("--gs-summary", nargs="+", metavar="CSV",
@@ -282,12 +286,11 @@ def recorded_cpu_configs():
         return None
 
 
-def layer_sweep(torch, bc, dev):
-    """Single block-sparse layers at their 2048x1024-frame shapes, 38 of 128 blocks
-    active (clustered): the stride-4 3x3 64->64 layer (256x512, 32-px blocks) and the
-    stride-16 sweep (64x128, 8-px blocks), 1x1 and 3x3 with Cin and Cout in {256, 512,
-    1024} (all nine pairs). Each is timed as a captured graph of 10 launches; FLOPs are
-    algorithmic (2*Cin*Cout*k*k per active output pixel)."""
+def sweep_layers(torch, bc, dev):
+    """The single-layer sweep's layers: the stride-4 3x3 64->64 layer (256x512, 32-px
+    blocks) and the stride-16 sweep (64x128, 8-px blocks), 1x1 and 3x3 with Cin and Cout
+    in {256, 512, 1024} (all nine pairs), on 38 of 128 clustered blocks. Yields (name,
+    call, algorithmic FLOPs, algorithmic bytes) per layer, its tensors on the device."""
     import numpy as np
 
     import synth
@@ -301,14 +304,28 @@ def layer_sweep(torch, bc, dev):
     idx = torch.empty(128, dtype=torch.int32, device=dev)
     cnt = torch.empty(1, dtype=torch.int32, device=dev)
     bc.bc_build_block_index(m, 1, (8, 16), idx, cnt)
-    out = {}
     r = synth.rng(synth.SEED_WEIGHT0)
+    n_act = int(mask.sum())
     for name, cin, cout, h, w, k in shapes:
         x = torch.from_numpy(synth.to_storage_bits(synth.normal(r, (1, h, w, cin)), "bf16").view(np.int16)).view(torch.bfloat16).to(dev)
         wt = torch.from_numpy(bc.bc_repack_weights(synth.he_normal(r, cout, cin, k, k), bc.BC_BF16).view(np.int16)).view(torch.bfloat16).to(dev)
         b = torch.zeros(cout, dtype=torch.float32, device=dev)
         y = torch.zeros((1, h, w, cout), dtype=torch.bfloat16, device=dev)
-        call = lambda: bc.bc_sparse_conv2d((k, k, 1, k // 2, 1), x, bc.BC_NHWC, wt, b, None, y, (8, 16), idx, cnt)
+        call = (lambda k=k, x=x, wt=wt, b=b, y=y: bc.bc_sparse_conv2d(
+            (k, k, 1, k // 2, 1), x, bc.BC_NHWC, wt, b, None, y, (8, 16), idx, cnt))
+        fl = 2.0 * cin * cout * k * k * h * w * n_act / mask.size
+        # algorithmic bytes: the active blocks' halo tiles, outputs and the weights, once
+        bh, bw = h // 8, w // 16
+        nb = n_act * ((bh + k - 1) * (bw + k - 1) * cin + bh * bw * cout) * 2 + cout * k * k * cin * 2
+        yield name, call, fl, nb
+
+
+def layer_sweep(torch, bc, dev):
+    """Single block-sparse layers at their 2048x1024-frame shapes (sweep_layers), each
+    timed as a captured graph of 10 launches; FLOPs are algorithmic (2*Cin*Cout*k*k per
+    active output pixel)."""
+    out = {}
+    for name, call, fl, nb in sweep_layers(torch, bc, dev):
         call()
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
@@ -324,16 +341,65 @@ def layer_sweep(torch, bc, dev):
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / 50
-        n_act = int(mask.sum())
-        fl = 2.0 * cin * cout * k * k * h * w * n_act / mask.size
-        # algorithmic bytes: the active blocks' halo tiles, outputs and the weights, once
-        bh, bw = h // 8, w // 16
-        nb = n_act * ((bh + k - 1) * (bw + k - 1) * cin + bh * bw * cout) * 2 + cout * k * k * cin * 2
         out[name] = {"us": round(us, 2), "tflops": round(fl / us / 1e6, 1),
                      "frac_of_mfma_peak": round(fl / us / 1e6 / PEAK_BF16_TFLOPS, 4),
                      "bytes": nb, "frac_of_hbm_peak": round(nb / us / 1e3 / PEAK_HBM_GBS, 4)}
         del g
     return out
+
+
+def pmc_layers(torch, bc, dev, reps):
+    """Counter run of the single-layer sweep: every layer of sweep_layers once to warm,
+    then `reps` more times, eager, so each dispatch is one layer call."""
+    for _, call, _, _ in sweep_layers(torch, bc, dev):
+        for _ in range(1 + reps):
+            call()
+        torch.cuda.synchronize()
+
+
+def layer_counter_summary(counter_csv, agent_csv):
+    """Text summary of a rocprofv3 --pmc run of `bench.py --pmc-layers N` with the
+    matrix-core and LDS counters of counter_summary. Per sweep layer, mean over the N
+    timed calls: duration, mfma_util (MFMA busy cycles over SIMDs x duration x peak
+    clock), rocprof's MfmaUtil / LdsUtil / LdsBankConflict, LDS instructions per
+    matrix-core instruction, and the matrix-core FLOPs seen over the algorithmic ones."""
+    import csv
+
+    agent = [r for r in csv.DictReader(open(agent_csv)) if r.get("Name", "").startswith("gfx")][0]
+    simds, clk = int(agent["Simd_Count"]), float(agent["Max_Engine_Clk_Fcompute"]) * 1e6
+    per = {}
+    for r in csv.DictReader(open(counter_csv)):
+        d = per.setdefault(int(r["Dispatch_Id"]), {
+            "name": r["Kernel_Name"],
+            "dur": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    conv = [per[k] for k in sorted(per) if "k_conv_" in per[k]["name"]]
+    shapes = [("3x3 64->64 @256x512", 64, 64, 256, 512, 3)]
+    for cin in (256, 512, 1024):
+        for cout in (256, 512, 1024):
+            for k in (1, 3):
+                shapes.append((f"{k}x{k} {cin}->{cout} @64x128", cin, cout, 64, 128, k))
+    if len(conv) % len(shapes):
+        raise SystemExit(f"{counter_csv}: {len(conv)} conv dispatches is not a whole number per layer")
+    calls = len(conv) // len(shapes)
+    out = [f"device: {simds} SIMDs, peak engine clock {clk / 1e9:.2f} GHz; one 16x16x32 bf16 MFMA "
+           f"holds a SIMD's matrix core for 16 cycles, so busy cycles x 16384 / 16 = FLOPs at peak",
+           f"{'layer':24s} {'us':>7s} {'mfma_util':>9s} {'MfmaUtil%':>9s} {'LdsUtil%':>8s} "
+           f"{'LdsBank%':>8s} {'lds/mfma':>8s} {'flop/algo':>9s}"]
+    for j, (name, cin, cout, h, w, k) in enumerate(shapes):
+        runs = conv[j * calls + 1:(j + 1) * calls]
+
+        def mean(key):
+            return sum(d[key] for d in runs) / len(runs)
+
+        fl = 2.0 * cin * cout * k * k * h * w * 38 / 128
+        dur = mean("dur")
+        out.append(f"{name:24s} {dur * 1e6:7.2f} {mean('SQ_VALU_MFMA_BUSY_CYCLES') / (simds * dur * clk):9.4f} "
+                   f"{mean('MfmaUtil'):9.2f} {mean('LdsUtil'):8.2f} {mean('LdsBankConflict'):8.3f} "
+                   f"{mean('SQ_INSTS_LDS') / mean('SQ_INSTS_VALU_MFMA_MOPS_BF16') * 32:8.3f} "
+                   f"{mean('SQ_INSTS_VALU_MFMA_MOPS_BF16') * 512 / fl:9.3f}")
+    out.append(f"conv_source_sha256={conv_source_sha()}")
+    return "\n".join(out)
 
 
 def vendor_dense_frame(torch, dev, layers):
@@ -1105,6 +1171,9 @@ def main():
     if args.counter_summary:
         print(counter_summary(*args.counter_summary))
         return
+    if args.layer_counter_summary:
+        print(layer_counter_summary(*args.layer_counter_summary))
+        return
     if args.gs_summary:
         print(gs_summary(*args.gs_summary))
         return
@@ -1125,6 +1194,10 @@ def main():
     if args.pmc_gather_scatter:
         from paper_2108_09376_amd import bc
         pmc_gather_scatter(torch, bc, dev)
+        return
+    if args.pmc_layers:
+        from paper_2108_09376_amd import bc
+        pmc_layers(torch, bc, dev, args.pmc_layers)
         return
     H, W, BLOCK = 1024, 2048, 128
     net = resnet.SparseResNet(50, H, W, BLOCK, device=dev)
