@@ -327,3 +327,72 @@ def test_errors_leave_buffers_untouched(B):
     torch.cuda.synchronize()
     assert bool((out == 0).all())
     buf.release()
+
+
+# ------------------------------------------------------------------ a3: seeded random sweep
+
+def _mask_pattern(kind, gh, gw, r):
+    """Execution grids of one image: Bernoulli(0.4), none, one block, checkerboard, the
+    border ring, every block."""
+    y, x = np.mgrid[0:gh, 0:gw]
+    m = {"bern": r.random((gh, gw)) < 0.4,
+         "empty": np.zeros((gh, gw), bool),
+         "one": (y == r.integers(gh)) & (x == r.integers(gw)),
+         "checker": (y + x) % 2 == 0,
+         "border": (y == 0) | (y == gh - 1) | (x == 0) | (x == gw - 1),
+         "full": np.ones((gh, gw), bool)}[kind]
+    return m.astype(np.uint8)[None]
+
+
+def _random_cases(count, seed=2108):
+    """Seeded layer configurations inside the supported space (Cout a multiple of 64;
+    Cin a multiple of 8, or the few-channel stem form; kernel edge 1, 3, 5 or 7;
+    stride 1 or 2; block edges 2-32 px, square or not, whose width divides 64), each
+    with a mask pattern and a storage format. The dense oracle's work stays under
+    about 1 GFLOP per case."""
+    r = np.random.default_rng(seed)
+    kinds = ["bern", "empty", "one", "checker", "border", "full"]
+    out = []
+    while len(out) < count:
+        k = int(r.choice([1, 3, 3, 3, 5, 7]))
+        s = int(r.choice([1, 2]))
+        if k == 7 or (k in (3, 5) and r.random() < 0.2):
+            cin = int(r.choice([3, 4]))                          # stem form
+        elif k == 1 and r.random() < 0.15:
+            cin = int(r.choice([3, 5]))
+        else:
+            cin = int(8 * r.integers(1, 41)) if r.random() < 0.6 else int(r.choice([64, 128, 256]))
+        cout = int(64 * r.integers(1, 4))
+        bw = int(r.choice([4, 8, 16, 32] if k <= 3 else [4, 8, 16]))
+        bh = int(r.choice([b for b in (bw // 2, bw, 2 * bw) if 2 <= b <= 32]))
+        gh, gw = int(r.integers(1, 5)), int(r.integers(1, 6))
+        ho, wo = gh * bh, gw * bw
+        if ho > 96 or wo > 160:
+            continue
+        if 2.0 * cin * cout * k * k * ho * wo > 1e9:
+            continue
+        out.append(dict(cin=cin, cout=cout, h=ho * s, w=wo * s, gh=gh, gw=gw, k=k, s=s,
+                        relu=bool(r.random() < 0.5), res=bool(r.random() < 0.5),
+                        mask=kinds[len(out) % len(kinds)], dtype=("bf16", "f16")[len(out) % 2],
+                        seed=int(r.integers(1 << 30))))
+    return out
+
+
+RANDOM_CASES = _random_cases(36)
+
+
+@pytest.mark.parametrize("c", RANDOM_CASES,
+                         ids=[f"r{i}_c{c['cin']}-{c['cout']}_k{c['k']}s{c['s']}_b{c['h'] // c['s'] // c['gh']}x"
+                              f"{c['w'] // c['s'] // c['gw']}_{c['mask']}_{c['dtype']}"
+                              for i, c in enumerate(RANDOM_CASES)])
+def test_conv_random_shapes_integer_exact(B, c):
+    """Small-integer operands on seeded random shapes: every partial sum is an integer
+    exact in fp32, so whatever the plan (tile shape, K split, stage grouping, stem or
+    general form) the output must equal the oracle's byte for byte, copied blocks
+    (NaN canaries) included."""
+    r = synth.rng(c["seed"])
+    mask = _mask_pattern(c["mask"], c["gh"], c["gw"], r)
+    case = (c["cin"], c["cout"], c["h"], c["w"], c["gh"], c["gw"], c["k"], c["s"], c["relu"],
+            c["res"], 0.0)
+    got, want, _, _ = _conv_case(B, c["dtype"], case, seed=c["seed"], integer=True, mask=mask)
+    assert np.array_equal(got, want)
