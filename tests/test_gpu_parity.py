@@ -396,3 +396,90 @@ def test_conv_random_shapes_integer_exact(B, c):
             c["res"], 0.0)
     got, want, _, _ = _conv_case(B, c["dtype"], case, seed=c["seed"], integer=True, mask=mask)
     assert np.array_equal(got, want)
+
+
+def _random_window_cases(count, seed, pool):
+    """Seeded window geometries (edge 1-7, stride 1 or 2, pad up to edge / 2), block
+    edges 2-16 px of the output, grids up to 4 x 5, channel counts and storage formats
+    (pooling: 16-bit channels-last with C a multiple of 8, or fp32 channels-first; the
+    gather takes any element size, layout and C), each with one of the mask patterns."""
+    r = np.random.default_rng(seed)
+    kinds = ["bern", "empty", "one", "checker", "border", "full"]
+    fmts = ([("bf16", True), ("f16", True), ("f32", False)] if pool else
+            [("bf16", True), ("f16", True), ("f32", False), ("f32", True)])
+    out = []
+    while len(out) < count:
+        k = int(r.integers(1, 8))
+        s = int(r.choice([1, 2]))
+        p = int(r.integers(0, k // 2 + 1))
+        bh, bw = int(r.choice([2, 4, 8, 16])), int(r.choice([2, 4, 8, 16]))
+        gh, gw = int(r.integers(1, 5)), int(r.integers(1, 6))
+        ho, wo = gh * bh, gw * bw
+        # input size giving exactly this output: (h + 2p - k) // s + 1 == ho
+        h, w = (ho - 1) * s + k - 2 * p, (wo - 1) * s + k - 2 * p
+        if h < 1 or w < 1:
+            continue
+        dtype, nhwc = fmts[len(out) % len(fmts)]
+        c = int(8 * r.integers(1, 9)) if pool and nhwc else int(r.integers(1, 41))
+        out.append(dict(k=k, s=s, p=p, h=h, w=w, gh=gh, gw=gw, c=c, dtype=dtype, nhwc=nhwc,
+                        mask=kinds[len(out) % len(kinds)], seed=int(r.integers(1 << 30))))
+    return out
+
+
+POOL_CASES = _random_window_cases(24, 2109, pool=True)
+
+
+@pytest.mark.parametrize("c", POOL_CASES,
+                         ids=[f"r{i}_k{c['k']}s{c['s']}p{c['p']}_{c['h']}x{c['w']}_g{c['gh']}x{c['gw']}_"
+                              f"c{c['c']}_{c['dtype']}{'' if c['nhwc'] else '_nchw'}_{c['mask']}"
+                              for i, c in enumerate(POOL_CASES)])
+def test_maxpool_random_shapes_bit_exact(B, c):
+    """Max pooling on seeded random windows and block grids: active blocks equal the
+    oracle's dense-then-select maximum, copied blocks keep their NaN canaries."""
+    r = synth.rng(c["seed"])
+    dtype, nhwc = c["dtype"], c["nhwc"]
+    x = synth.to_storage_bits(synth.normal(r, (1, c["c"], c["h"], c["w"])), dtype)
+    ho = oracle.out_size(c["h"], c["k"], c["s"], c["p"])
+    wo = oracle.out_size(c["w"], c["k"], c["s"], c["p"])
+    prev = synth.nan_canaries(r, (1, c["c"], ho, wo), dtype)
+    mask = _mask_pattern(c["mask"], c["gh"], c["gw"], r)
+    want = oracle.sparse_maxpool2d(x, mask, prev, dtype, c["k"], c["s"], c["p"])
+    idx, cnt, _ = _index(B, mask)
+    out = to_dev(prev, dtype, nhwc)
+    B.bc_sparse_maxpool2d((c["k"], c["k"], c["s"], c["p"], 0), to_dev(x, dtype, nhwc),
+                          B.BC_NHWC if nhwc else B.BC_NCHW, out, (c["gh"], c["gw"]), idx, cnt)
+    assert np.array_equal(from_dev(out, nhwc), want)
+
+
+GATHER_CASES = _random_window_cases(24, 2110, pool=False)
+
+
+@pytest.mark.parametrize("c", GATHER_CASES,
+                         ids=[f"r{i}_k{c['k']}s{c['s']}p{c['p']}_{c['h']}x{c['w']}_g{c['gh']}x{c['gw']}_"
+                              f"c{c['c']}_{c['dtype']}{'' if c['nhwc'] else '_nchw'}_{c['mask']}"
+                              for i, c in enumerate(GATHER_CASES)])
+def test_gather_random_shapes_bit_exact(B, c):
+    """Standalone halo gather on seeded random windows and block grids: every active
+    block's tile equals the oracle's, out-of-image taps carry the pad value, and the
+    slots past the active count stay untouched."""
+    r = synth.rng(c["seed"])
+    dtype, nhwc, k, s, p = c["dtype"], c["nhwc"], c["k"], c["s"], c["p"]
+    gh, gw = c["gh"], c["gw"]
+    x = synth.to_storage_bits(synth.normal(r, (1, c["c"], c["h"], c["w"])), dtype)
+    mask = _mask_pattern(c["mask"], gh, gw, r)
+    idx_np, cnt_np = oracle.block_index(mask)
+    bh = oracle.out_size(c["h"], k, s, p) // gh
+    bw = oracle.out_size(c["w"], k, s, p) // gw
+    pad_value = -np.inf if k % 2 else 0.0
+    pad_bits = synth.to_storage_bits(np.array([pad_value], np.float32), dtype)[0]
+    want = oracle.gather_halo(x, idx_np, gh, gw, bh, bw, k, k, s, p, pad_bits)
+    idx, cnt, _ = _index(B, mask)
+    th, tw = (bh - 1) * s + k, (bw - 1) * s + k
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dtype]
+    packed = torch.zeros((idx.numel(), th, tw, c["c"]), dtype=tdt, device="cuda")
+    B.bc_gather_halo(to_dev(x, dtype, nhwc), B.BC_NHWC if nhwc else B.BC_NCHW, (gh, gw),
+                     (k, k, s, p, 0), pad_value, idx, cnt, packed)
+    got = packed.cpu()
+    got = got.view(torch.int16).numpy().view(np.uint16) if dtype != "f32" else got.numpy().view(np.uint32)
+    assert np.array_equal(got[:cnt_np], want)
+    assert not got[cnt_np:].any()
