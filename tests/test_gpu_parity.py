@@ -483,3 +483,37 @@ def test_gather_random_shapes_bit_exact(B, c):
     got = got.view(torch.int16).numpy().view(np.uint16) if dtype != "f32" else got.numpy().view(np.uint32)
     assert np.array_equal(got[:cnt_np], want)
     assert not got[cnt_np:].any()
+
+
+SCATTER_CASES = _random_window_cases(16, 2111, pool=False)
+
+
+@pytest.mark.parametrize("c", SCATTER_CASES,
+                         ids=[f"r{i}_g{c['gh']}x{c['gw']}_c{c['c']}_{c['dtype']}"
+                              f"{'' if c['nhwc'] else '_nchw'}_{c['mask']}"
+                              for i, c in enumerate(SCATTER_CASES)])
+def test_scatter_random_shapes_bit_exact(B, c):
+    """Standalone scatter on seeded random block grids, block edges, channel counts and
+    formats: active blocks take the packed tiles, every other element keeps its NaN
+    canary bit for bit."""
+    r = synth.rng(c["seed"])
+    dtype, nhwc, gh, gw = c["dtype"], c["nhwc"], c["gh"], c["gw"]
+    h = oracle.out_size(c["h"], c["k"], c["s"], c["p"])
+    w = oracle.out_size(c["w"], c["k"], c["s"], c["p"])
+    bh, bw = h // gh, w // gw
+    dst = synth.nan_canaries(r, (1, c["c"], h, w), dtype)
+    mask = _mask_pattern(c["mask"], gh, gw, r)
+    idx_np, cnt_np = oracle.block_index(mask)
+    packed_bits = synth.to_storage_bits(synth.normal(r, (cnt_np, bh, bw, c["c"])), dtype)
+    want = oracle.scatter_blocks(packed_bits, idx_np, gh, gw, dst)
+    idx, cnt, _ = _index(B, mask)
+    full = np.zeros((idx.numel(), bh, bw, c["c"]), packed_bits.dtype)
+    full[:cnt_np] = packed_bits
+    if dtype == "f32":
+        pk = torch.from_numpy(full.view(np.float32)).cuda()
+    else:
+        tdt = {"bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+        pk = torch.from_numpy(full.view(np.int16)).view(tdt).cuda()
+    d = to_dev(dst, dtype, nhwc)
+    B.bc_scatter_blocks(pk, idx, cnt, (gh, gw), d, B.BC_NHWC if nhwc else B.BC_NCHW)
+    assert np.array_equal(from_dev(d, nhwc), want)
