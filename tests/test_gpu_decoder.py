@@ -276,3 +276,61 @@ def test_spp_no_block_and_every_block(B):
     torch.cuda.synchronize()
     got = from_dev(out)
     assert np.array_equal(got[:, :c], x) and not np.isnan(oracle.value(got, "bf16")).any()
+
+
+def _mask_pattern(kind, n, gh, gw, r):
+    """Execution grids: Bernoulli(0.4), none, one block, checkerboard, border ring, all."""
+    y, x = np.mgrid[0:gh, 0:gw]
+    one = {"bern": lambda: r.random((gh, gw)) < 0.4,
+           "empty": lambda: np.zeros((gh, gw), bool),
+           "one": lambda: (y == r.integers(gh)) & (x == r.integers(gw)),
+           "checker": lambda: (y + x) % 2 == 0,
+           "border": lambda: (y == 0) | (y == gh - 1) | (x == 0) | (x == gw - 1),
+           "full": lambda: np.ones((gh, gw), bool)}[kind]
+    return np.stack([one() for _ in range(n)]).astype(np.uint8)
+
+
+def _random_upsample_cases(count, seed=2112):
+    """Seeded coarse maps (1-24 x 1-24), grids dividing the 2x output, channel counts and
+    formats (16-bit channels-last with C a multiple of 8, or fp32 channels-first), skip
+    and ReLU on or off, each under one mask pattern."""
+    r = np.random.default_rng(seed)
+    kinds = ["bern", "empty", "one", "checker", "border", "full"]
+    fmts = [("bf16", True), ("f16", True), ("f32", False)]
+    out = []
+    while len(out) < count:
+        hc, wc = int(r.integers(1, 25)), int(r.integers(1, 25))
+        gh = int(r.choice([d for d in range(1, 9) if (2 * hc) % d == 0]))
+        gw = int(r.choice([d for d in range(1, 9) if (2 * wc) % d == 0]))
+        dtype, nhwc = fmts[len(out) % len(fmts)]
+        c = int(8 * r.integers(1, 9)) if nhwc else int(r.integers(1, 20))
+        out.append(dict(dtype=dtype, nhwc=nhwc, n=int(r.integers(1, 3)), c=c, hc=hc, wc=wc,
+                        grid=(gh, gw), skip=bool(r.random() < 0.7), relu=bool(r.random() < 0.5),
+                        mask=kinds[len(out) % len(kinds)], seed=int(r.integers(1 << 30))))
+    return out
+
+
+UPSAMPLE_CASES = _random_upsample_cases(18)
+
+
+@pytest.mark.parametrize("c", UPSAMPLE_CASES,
+                         ids=[f"r{i}_{c['dtype']}{'' if c['nhwc'] else '_nchw'}_n{c['n']}_c{c['c']}_"
+                              f"{c['hc']}x{c['wc']}_g{c['grid'][0]}x{c['grid'][1]}_{c['mask']}"
+                              for i, c in enumerate(UPSAMPLE_CASES)])
+def test_upsample_add_random_shapes(B, c):
+    """Upsample-and-add on seeded random shapes and grids: copied blocks bit for bit,
+    executed blocks within the storage format's bound of the fp64 oracle."""
+    r = synth.rng(c["seed"])
+    dtype, nhwc, n, ch, hc, wc = c["dtype"], c["nhwc"], c["n"], c["c"], c["hc"], c["wc"]
+    gh, gw = c["grid"]
+    coarse = synth.to_storage_bits(synth.normal(r, (n, ch, hc, wc)), dtype)
+    sk = synth.to_storage_bits(synth.normal(r, (n, ch, 2 * hc, 2 * wc)), dtype) if c["skip"] else None
+    prev = synth.nan_canaries(r, (n, ch, 2 * hc, 2 * wc), dtype)
+    mask = _mask_pattern(c["mask"], n, gh, gw, r)
+    want = oracle.sparse_upsample_add(coarse, sk, mask, prev, dtype, c["relu"])
+    idx, cnt = _index(B, mask)
+    out = to_dev(prev, dtype, nhwc)
+    B.bc_sparse_upsample_add(to_dev(coarse, dtype, nhwc), B.BC_NHWC if nhwc else B.BC_NCHW,
+                             to_dev(sk, dtype, nhwc) if c["skip"] else None, out, (gh, gw),
+                             int(c["relu"]), idx, cnt)
+    _check_merge(from_dev(out, nhwc), want, mask, dtype)

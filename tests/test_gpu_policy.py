@@ -174,3 +174,50 @@ def test_rewards_without_loss(B):
     want, _, m = P.block_rewards(ig.cpu().numpy(), mask.cpu().numpy(), 0.3, 5.0, 0.9, [0.5])
     assert max_abs_rel(reward.cpu().numpy(), want) <= TOL_F32
     assert abs(float(mavg.item()) - m[0]) <= 1e-6
+
+
+def _random_state_cases(count, seed=2113):
+    """Seeded frame-state shapes: batch 1-2, 1-8 channels, block edges 1-12 px on grids up
+    to 6 x 7, every storage format in either layout, each under one mask pattern."""
+    r = np.random.default_rng(seed)
+    kinds = ["bern", "empty", "one", "checker", "border", "full"]
+    fmts = [("bf16", True), ("f16", True), ("f32", False), ("f32", True), ("bf16", False), ("f16", False)]
+    out = []
+    for i in range(count):
+        gh, gw = int(r.integers(1, 7)), int(r.integers(1, 8))
+        bh, bw = int(r.integers(1, 13)), int(r.integers(1, 13))
+        dtype, nhwc = fmts[i % len(fmts)]
+        out.append(dict(dtype=dtype, nhwc=nhwc, shape=(int(r.integers(1, 3)), int(r.integers(1, 9)),
+                                                      gh * bh, gw * bw),
+                        grid=(gh, gw), mask=kinds[i % len(kinds)], seed=int(r.integers(1 << 30))))
+    return out
+
+
+STATE_CASES = _random_state_cases(18)
+
+
+@pytest.mark.parametrize("c", STATE_CASES,
+                         ids=[f"r{i}_{c['dtype']}{'' if c['nhwc'] else '_nchw'}_{'x'.join(map(str, c['shape']))}_"
+                              f"g{c['grid'][0]}x{c['grid'][1]}_{c['mask']}" for i, c in enumerate(STATE_CASES)])
+def test_frame_state_random_shapes(B, c):
+    """Frame state on seeded random shapes, grids and formats: executed blocks take the
+    frame's bits, every other element keeps its NaN canary."""
+    r = synth.rng(c["seed"])
+    dtype, nhwc, shape = c["dtype"], c["nhwc"], c["shape"]
+    gh, gw = c["grid"]
+    frame = synth.to_storage_bits(synth.normal(r, shape), dtype)
+    state = synth.nan_canaries(r, shape, dtype)
+    y, x = np.mgrid[0:gh, 0:gw]
+    pick = {"bern": lambda: r.random((gh, gw)) < 0.4, "empty": lambda: np.zeros((gh, gw), bool),
+            "one": lambda: (y == r.integers(gh)) & (x == r.integers(gw)),
+            "checker": lambda: (y + x) % 2 == 0,
+            "border": lambda: (y == 0) | (y == gh - 1) | (x == 0) | (x == gw - 1),
+            "full": lambda: np.ones((gh, gw), bool)}[c["mask"]]
+    mask = np.stack([pick() for _ in range(shape[0])]).astype(np.uint8)
+    want = P.update_frame_state(frame, state, mask, "nchw")
+    idx = torch.empty(mask.size, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(1, dtype=torch.int32, device="cuda")
+    B.bc_build_block_index(torch.from_numpy(mask).cuda(), shape[0], (gh, gw), idx, cnt)
+    f, s = to_dev(frame, dtype, nhwc), to_dev(state, dtype, nhwc)
+    B.bc_update_frame_state(f, s, B.BC_NHWC if nhwc else B.BC_NCHW, (gh, gw), idx, cnt)
+    assert np.array_equal(from_dev(s, nhwc), want)
